@@ -1,0 +1,223 @@
+"""Seeded generators for the SpMM workloads.
+
+Shapes follow the decode-phase setting of Section 5.1: the sparse weight W is
+M x K, the dense activation X is K x N with N the batch of tokens, and the
+product Y is M x N. Storage conventions used throughout this repository:
+
+* W: row-major M x K fp16 (``nn.Linear.weight`` layout), returned as uint16
+  bit patterns.
+* mask: row-major M x K uint8, nonzero = the weight is kept.
+* X: token-major, i.e. an N x K array whose row n is column n of the logical
+  K x N matrix (the ``[B, H]`` activation of Section 2.1), fp16 bit patterns.
+
+Every draw comes from ``numpy.random.default_rng(SeedSequence([2607, cfg_id,
+stream, n_or_0]))`` with stream 0 = W values, 1 = mask / column scales,
+2 = X. Samples are drawn in float64 and cast to fp16 with round-to-nearest-even.
+Row draws are taken in fixed chunks of ``ROW_CHUNK`` rows so that memory stays
+bounded; the chunking is part of the definition of each instance.
+
+Pruning is magnitude based (Section 5.3 prunes with Wanda; real weights are not
+available here, so magnitudes of synthetic weights stand in):
+
+* per row: keep the ``keep_count(K, s)`` largest |w| of each row, ranking by the
+  fp16 magnitude bits, ties to the lower column index;
+* global: the same over the whole matrix, ties to the lower row-major index;
+* per row with column scale (the 13B FFN pair): rank by |w| * s_k where s_k is a
+  log-normal scale of input feature k, so the density of W's columns varies.
+"""
+from __future__ import annotations
+
+import dataclasses
+import hashlib
+
+import numpy as np
+
+ROW_CHUNK = 1024
+BASE_SEED = 2607
+
+
+def seed_for(cfg_id: int, stream: int, n_or_0: int = 0) -> np.random.Generator:
+    return np.random.default_rng(np.random.SeedSequence([BASE_SEED, cfg_id, stream, n_or_0]))
+
+
+def keep_count(K: int, sparsity_pct: int) -> int:
+    """Kept entries out of K at ``sparsity_pct`` percent sparsity: round((100-s)K/100), halves up."""
+    return ((100 - sparsity_pct) * K * 2 + 100) // 200
+
+
+def _f16_bits(a: np.ndarray) -> np.ndarray:
+    return np.ascontiguousarray(a.astype(np.float16)).view(np.uint16)
+
+
+def draw_weights(cfg_id: int, M: int, K: int, dist: str, scale: float) -> np.ndarray:
+    """M x K fp16 bit patterns, drawn ROW_CHUNK rows at a time."""
+    rng = seed_for(cfg_id, 0)
+    out = np.empty((M, K), dtype=np.uint16)
+    for r0 in range(0, M, ROW_CHUNK):
+        r1 = min(M, r0 + ROW_CHUNK)
+        if dist == "normal":
+            v = rng.normal(0.0, scale, size=(r1 - r0, K))
+        elif dist == "student_t4":
+            v = rng.standard_t(4, size=(r1 - r0, K)) * scale
+        else:
+            raise ValueError(dist)
+        out[r0:r1] = _f16_bits(v)
+    return out
+
+
+def make_x(cfg_id: int, K: int, N: int) -> np.ndarray:
+    """N x K (token-major) fp16 bit patterns with entries N(0, 1)."""
+    rng = seed_for(cfg_id, 2, N)
+    return _f16_bits(rng.normal(0.0, 1.0, size=(N, K)))
+
+
+def _magnitude_bits(W: np.ndarray) -> np.ndarray:
+    return W & np.uint16(0x7FFF)
+
+
+def prune_per_row(score: np.ndarray, keep: int) -> np.ndarray:
+    """Keep the ``keep`` largest scores of each row (ties: lower column index)."""
+    M, K = score.shape
+    mask = np.zeros((M, K), dtype=np.uint8)
+    if keep <= 0:
+        return mask
+    if keep >= K:
+        mask[:] = 1
+        return mask
+    for r0 in range(0, M, ROW_CHUNK):
+        s = score[r0:r0 + ROW_CHUNK]
+        srt = np.sort(s, axis=1)
+        t = srt[:, K - keep][:, None]
+        gt = s > t
+        eq = s == t
+        need = keep - gt.sum(axis=1, keepdims=True)
+        take_eq = eq & (np.cumsum(eq, axis=1) <= need)
+        mask[r0:r0 + ROW_CHUNK] = gt | take_eq
+    return mask
+
+
+def prune_global(W: np.ndarray, keep: int) -> np.ndarray:
+    """Keep the ``keep`` largest |w| of the whole matrix (ties: lower row-major index)."""
+    M, K = W.shape
+    mag = _magnitude_bits(W)
+    hist = np.bincount(mag.ravel(), minlength=1 << 15).astype(np.int64)
+    # number of entries with magnitude >= t, for every t
+    ge = np.cumsum(hist[::-1])[::-1]
+    # threshold bin t: count(mag > t) < keep <= count(mag >= t)
+    t = int(np.nonzero(ge >= keep)[0].max()) if keep > 0 else (1 << 15)
+    mask = np.zeros((M, K), dtype=np.uint8)
+    if keep <= 0:
+        return mask
+    n_gt = int(ge[t + 1]) if t + 1 < len(ge) else 0
+    need = keep - n_gt
+    taken = 0
+    for r0 in range(0, M, ROW_CHUNK):
+        m = mag[r0:r0 + ROW_CHUNK]
+        gt = m > t
+        eq = m == t
+        flat_eq = eq.ravel()
+        c = np.cumsum(flat_eq) + taken
+        take = (flat_eq & (c <= need)).reshape(eq.shape)
+        taken = min(need, taken + int(flat_eq.sum()))
+        mask[r0:r0 + ROW_CHUNK] = gt | take
+    return mask
+
+
+@dataclasses.dataclass
+class Instance:
+    name: str
+    cfg_id: int
+    M: int
+    K: int
+    N: int
+    sparsity_pct: int
+    prune: str
+    W: np.ndarray  # uint16 M x K
+    mask: np.ndarray  # uint8 M x K
+    X: np.ndarray  # uint16 N x K
+
+    def digests(self) -> dict:
+        return {k: hashlib.sha256(np.ascontiguousarray(getattr(self, k)).tobytes()).hexdigest()
+                for k in ("W", "mask", "X")}
+
+    @property
+    def nnz(self) -> int:
+        return int(np.count_nonzero(self.mask))
+
+
+# Layer shapes of the workloads. cfg_id keys the seeds.
+CONFIGS = {
+    "tiny": dict(cfg_id=1, M=1024, K=1024, dist="normal", scale=0.02, prune="bernoulli",
+                 sparsity=(50,), Ns=(16,)),
+    "attn13b": dict(cfg_id=2, M=5120, K=5120, dist="normal", scale=0.02, prune="row",
+                    sparsity=(50,), Ns=(8, 16, 32)),
+    "ffn13b_up": dict(cfg_id=31, M=13824, K=5120, dist="normal", scale=0.02, prune="row_colscale",
+                      sparsity=(50,), Ns=(16, 64)),
+    "ffn13b_down": dict(cfg_id=32, M=5120, K=13824, dist="normal", scale=0.02, prune="row_colscale",
+                        sparsity=(50,), Ns=(16, 64)),
+    "ffn66b": dict(cfg_id=4, M=36864, K=9216, dist="normal", scale=0.02, prune="global",
+                   sparsity=(60, 50), Ns=(16, 64, 128)),
+    "ffn70b": dict(cfg_id=5, M=28672, K=8192, dist="student_t4", scale=0.02, prune="row",
+                   sparsity=(40, 50, 60, 70), Ns=(8, 16, 32, 64, 128, 256)),
+}
+
+
+def make_mask(cfg: dict, W: np.ndarray, sparsity_pct: int) -> np.ndarray:
+    M, K = W.shape
+    kind = cfg["prune"]
+    if kind == "bernoulli":
+        rng = seed_for(cfg["cfg_id"], 1)
+        mask = np.empty((M, K), dtype=np.uint8)
+        for r0 in range(0, M, ROW_CHUNK):
+            r1 = min(M, r0 + ROW_CHUNK)
+            mask[r0:r1] = rng.random((r1 - r0, K)) < (100 - sparsity_pct) / 100.0
+        return mask
+    if kind == "row":
+        return prune_per_row(_magnitude_bits(W), keep_count(K, sparsity_pct))
+    if kind == "row_colscale":
+        rng = seed_for(cfg["cfg_id"], 1)
+        s = rng.lognormal(0.0, 0.5, size=K)
+        absw = np.abs(W.view(np.float16).astype(np.float64))
+        return prune_per_row(absw * s[None, :], keep_count(K, sparsity_pct))
+    if kind == "global":
+        return prune_global(W, keep_count(M * K, sparsity_pct))
+    raise ValueError(kind)
+
+
+def make_instance(name: str, N: int, sparsity_pct: int | None = None) -> Instance:
+    cfg = CONFIGS[name]
+    s = cfg["sparsity"][0] if sparsity_pct is None else sparsity_pct
+    W = draw_weights(cfg["cfg_id"], cfg["M"], cfg["K"], cfg["dist"], cfg["scale"])
+    mask = make_mask(cfg, W, s)
+    X = make_x(cfg["cfg_id"], cfg["K"], N)
+    return Instance(name=name, cfg_id=cfg["cfg_id"], M=cfg["M"], K=cfg["K"], N=N,
+                    sparsity_pct=s, prune=cfg["prune"], W=W, mask=mask, X=X)
+
+
+def instance_list():
+    """(name, N, sparsity) for every instance of the workload set."""
+    out = []
+    for name, cfg in CONFIGS.items():
+        for s in cfg["sparsity"]:
+            for N in cfg["Ns"]:
+                out.append((name, N, s))
+    return out
+
+
+def make_random(M: int, K: int, N: int, density: float, seed: int, scale: float = 0.02,
+                x_scale: float = 1.0):
+    """Small ad-hoc case: W ~ N(0, scale), Bernoulli(density) mask, X ~ N(0, x_scale)."""
+    rng = np.random.default_rng(np.random.SeedSequence([BASE_SEED, 999, seed, M, K, N]))
+    W = _f16_bits(rng.normal(0.0, scale, size=(M, K)))
+    mask = (rng.random((M, K)) < density).astype(np.uint8)
+    X = _f16_bits(rng.normal(0.0, x_scale, size=(N, K)))
+    return W, mask, X
+
+
+def make_small_int(M: int, K: int, N: int, density: float, seed: int, lo: int = -3, hi: int = 3):
+    """Small-integer W and X (exactly representable in fp16), Bernoulli(density) mask."""
+    rng = np.random.default_rng(np.random.SeedSequence([BASE_SEED, 998, seed, M, K, N]))
+    W = _f16_bits(rng.integers(lo, hi + 1, size=(M, K)).astype(np.float64))
+    mask = (rng.random((M, K)) < density).astype(np.uint8)
+    X = _f16_bits(rng.integers(lo, hi + 1, size=(N, K)).astype(np.float64))
+    return W, mask, X
