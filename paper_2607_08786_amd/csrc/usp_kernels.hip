@@ -1,0 +1,617 @@
+// usp_kernels.hip -- gfx950 kernels of the sparse product and their launchers.
+//
+// Work decomposition. A workgroup is 4 wavefronts; wavefront w owns row block
+// 4 rg + w of a row group rg (64 rows), and the 4 wavefronts walk the same
+// 256-column tiles in lockstep. The work is the sequence of units
+// (row group, column tile) in row-group-major order; the grid is persistent
+// (a fixed number of workgroups per CU) and workgroup w takes the contiguous
+// units [w U / G, (w+1) U / G), so every workgroup streams the same number of
+// tiles. A row group whose columns are split over several workgroups is
+// finished by whichever of them arrives last (see below).
+// Per tile:
+//   * the workgroup stages the X tile (N tokens x 256 columns, fp16) into LDS
+//     once; all 4 wavefronts read their MFMA B operands from it;
+//   * each wavefront stages its own compressed tile record into its LDS region;
+//     the next two tiles' records and X tiles are already being fetched into
+//     registers while the current one is decoded;
+//   * per 32-column step, a wavefront prefix sum of the lanes' kept counts gives
+//     each lane the start of its packed values (the decode is a prefix sum over
+//     the metadata, as the paper's PDD decode in Section 4.3 is); three packed
+//     DPP scans per tile cover all 8 steps;
+//   * each lane expands its 8 positions of the step into the 16 x 32 fp16 A
+//     operand: two nibble expansions, each a funnel shift (v_alignbyte) of three
+//     LDS dwords plus two byte permutes (v_perm) driven by a 16-entry selector
+//     table;
+//   * v_mfma_f32_16x16x32_f16 accumulates in fp32 (the dense-contraction part,
+//     Section 4.3).
+// Epilogue of a row group: fp32 -> fp16 with round to nearest even. When the
+// row group's columns were split, each contributing workgroup writes its fp32
+// partial sums with device-coherent stores and bumps the row group's counter;
+// the last to arrive reads every partial with device-coherent loads, sums them
+// in a fixed order (bitwise reproducible, no floating-point atomics), stores Y
+// and resets the counter to zero for the next call. No workgroup waits on
+// another.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+
+#include "usp_internal.h"
+
+namespace usp {
+namespace {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t v4u32 __attribute__((ext_vector_type(4)));
+
+// Word 3 of a raw buffer resource on gfx9-class targets (untyped 32-bit data).
+constexpr int kBufferRsrcWord3 = 0x00020000;
+// Cache policy with the device-scope bit (sc1): coherent across the XCDs' L2s.
+constexpr int kCachePolicyDevice = 16;
+
+constexpr int kWaves = 4;                              // row blocks per workgroup
+constexpr int kThreads = kWaves * kLanes;              // 256
+constexpr int kWRegionBytes = kMaxValBytes;            // 8 KB per wavefront (8 KB aligned)
+constexpr int kXRowBytes = kTileK * 2 + 16;            // 528: padded token row of the X tile
+constexpr int kMaxNT = 4;                              // 16-token blocks per pass (N <= 64)
+constexpr int kWgsPerCu = 3;                           // persistent workgroups per CU
+
+struct SpmmArgs {
+    const uint8_t *stream;
+    const uint32_t *off;
+    int64_t M, K, RB, KT;
+    const uint16_t *X;
+    int64_t ldx;
+    uint16_t *Y;
+    int64_t ldy;
+    int N;            // tokens of this pass (<= 16 * NT)
+    int64_t units;    // row groups * KT
+    int64_t maxseg;   // partial slots per row group
+    float *ws;        // partials [row group][slot][N][64], or null when no row group is split
+    uint32_t *cnt;    // arrival counters, one per row group (zero between calls)
+    int x_vec;        // X chunks may be read as 16-byte vectors
+    int y_vec;        // Y may be written as 8-byte vectors
+};
+
+// Selector pair for expanding nibble `n` (positions 0..3) from the 4 packed
+// halfs (c0,c1 | c2,c3) held in x0 | x1: output half j takes c_rank(j) when bit
+// j is set and zero (selector byte 0x0c) otherwise.
+__device__ inline uint2 nibble_selectors(uint32_t n) {
+    uint32_t sel[2] = {0x0c0c0c0cu, 0x0c0c0c0cu};
+    uint32_t r = 0;
+    for (int j = 0; j < 4; ++j) {
+        if (n & (1u << j)) {
+            const uint32_t pair = (2 * r) | ((2 * r + 1) << 8);
+            const int sh = 16 * (j & 1);
+            sel[j >> 1] = (sel[j >> 1] & ~(0xFFFFu << sh)) | (pair << sh);
+            ++r;
+        }
+    }
+    return make_uint2(sel[0], sel[1]);
+}
+
+// The LDS words one step's decode needs: for each of the two nibbles, the three
+// dwords holding its packed values and its selector pair, plus the byte
+// offsets of both starts. Reading them for step s + 1 before finishing step s
+// hides the LDS latency.
+struct StepWords {
+    uint32_t e[6];
+    uint2 sel[2];
+    uint32_t hb[2];
+};
+
+typedef const __attribute__((address_space(3))) uint32_t lds_u32;
+
+// Byte address of an LDS object (LDS addresses are 32-bit).
+__device__ inline uint32_t lds_address(const void *p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
+
+// region_base: LDS address of the wavefront's 8 KB-aligned region, so adding
+// the masked offset is a single OR.
+__device__ inline void read_nibble(uint32_t region_base, uint32_t hb, uint32_t idx8, const uint8_t *lut,
+                                   uint32_t *e, uint2 &sel) {
+    lds_u32 *d = (lds_u32 *)(uintptr_t)((hb & (kWRegionBytes - 4)) | region_base);
+    e[0] = d[0];
+    e[1] = d[1];
+    e[2] = d[2];
+    sel = *reinterpret_cast<const uint2 *>(lut + idx8);
+}
+
+// Expands one nibble whose packed values start at byte hb (even) from its three
+// dwords: a funnel shift aligns the 4 candidate halfs, then two byte permutes
+// place them (or zeros) at the nibble's 4 positions.
+__device__ inline void finish_nibble(const uint32_t *e, uint2 sel, uint32_t hb, uint32_t &o0, uint32_t &o1) {
+    const uint32_t x0 = __builtin_amdgcn_alignbyte(e[1], e[0], hb);  // uses hb & 3 (0 or 2)
+    const uint32_t x1 = __builtin_amdgcn_alignbyte(e[2], e[1], hb);
+    o0 = __builtin_amdgcn_perm(x1, x0, sel.x);
+    o1 = __builtin_amdgcn_perm(x1, x0, sel.y);
+}
+
+// Inclusive prefix sum over the 64 lanes of a wavefront (DPP row shifts and
+// row broadcasts, 7 adds).
+__device__ inline uint32_t wave_inclusive_scan(uint32_t v) {
+    v += __builtin_amdgcn_update_dpp(0u, v, 0x111, 0xF, 0xF, true);   // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0u, v, 0x112, 0xF, 0xF, true);   // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0u, v, 0x114, 0xF, 0xF, true);   // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0u, v, 0x118, 0xF, 0xF, true);   // row_shr:8
+    v += __builtin_amdgcn_update_dpp(0u, v, 0x142, 0xA, 0xF, false);  // row_bcast:15
+    v += __builtin_amdgcn_update_dpp(0u, v, 0x143, 0xC, 0xF, false);  // row_bcast:31
+    return v;
+}
+
+// Number of set bits of each byte of x, one count per byte.
+__device__ inline uint32_t byte_popcounts(uint32_t x) {
+    x = x - ((x >> 1) & 0x55555555u);
+    x = (x & 0x33333333u) + ((x >> 2) & 0x33333333u);
+    return (x + (x >> 4)) & 0x0F0F0F0Fu;
+}
+
+// Per-tile decode state of one lane: exclusive prefix (over lanes) of the kept
+// counts of every step, as three words of 10-bit fields, and the start (in
+// halfs) of every step's block of values.
+struct StepOffsets {
+    uint32_t excl[3];
+    uint32_t base[kSteps];  // wavefront-uniform
+};
+
+__device__ inline StepOffsets step_offsets(uint2 msk) {
+    const uint32_t bl = byte_popcounts(msk.x), bh = byte_popcounts(msk.y);
+    uint32_t w[3];
+    w[0] = (bl & 0xFFu) | ((bl & 0xFF00u) << 2) | ((bl & 0xFF0000u) << 4);
+    w[1] = (bl >> 24) | ((bh & 0xFFu) << 10) | ((bh & 0xFF00u) << 12);
+    w[2] = ((bh >> 16) & 0xFFu) | ((bh >> 24) << 10);
+    StepOffsets o;
+    uint32_t run = 0;
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+        const uint32_t inc = wave_inclusive_scan(w[i]);
+        o.excl[i] = inc - w[i];
+        const uint32_t tot = __builtin_amdgcn_readlane(inc, 63);
+#pragma unroll
+        for (int f = 0; f < 3; ++f) {
+            const int st = 3 * i + f;
+            if (st < kSteps) {
+                o.base[st] = run;
+                run += (tot >> (10 * f)) & 0x3FFu;
+            }
+        }
+    }
+    return o;
+}
+
+// Issues the LDS reads of step s of the staged tile.
+// tlo/thi: mask bytes of the step's low / high nibbles pre-scaled by 8.
+__device__ inline StepWords read_step(uint32_t region, const uint8_t *lut, const StepOffsets &so,
+                                      uint32_t tlo, uint32_t thi, int s) {
+    StepWords w;
+    const uint32_t P = (so.excl[s / 3] >> (10 * (s % 3))) & 0x3FFu;
+    const int sh = 8 * (s & 3);
+    const uint32_t i0 = (tlo >> sh) & 0xFFu, i1 = (thi >> sh) & 0xFFu;
+    w.hb[0] = (P + so.base[s]) << 1;
+    w.hb[1] = w.hb[0] + 2u * (uint32_t)__builtin_popcount(i0);
+    read_nibble(region, w.hb[0], i0, lut, w.e, w.sel[0]);
+    read_nibble(region, w.hb[1], i1, lut, w.e + 3, w.sel[1]);
+    return w;
+}
+
+// The A operand (8 halfs) of a step from its LDS words.
+__device__ inline half8 finish_step(const StepWords &w) {
+    uint4 a;
+    finish_nibble(w.e, w.sel[0], w.hb[0], a.x, a.y);
+    finish_nibble(w.e + 3, w.sel[1], w.hb[1], a.z, a.w);
+    return __builtin_bit_cast(half8, a);
+}
+
+__device__ inline half8 decode_step(uint32_t region, const uint8_t *lut, const StepOffsets &so,
+                                    uint32_t tlo, uint32_t thi, int s) {
+    return finish_step(read_step(region, lut, so, tlo, thi, s));
+}
+
+// One 16-byte chunk X[n][k..k+7] of the X tile, zero outside N x K.
+// XFAST: X is 16-byte aligned, ldx and K are multiples of 8, so a chunk is
+// either entirely inside or entirely outside; the load is issued
+// unconditionally (from a valid address) and zeroed afterwards, which keeps
+// the number of loads per tile fixed. Otherwise element-wise guarded loads.
+template <bool XFAST>
+__device__ inline uint4 load_x_chunk(const SpmmArgs &a, int n, int64_t k) {
+    const bool inside = n < a.N && k < a.K;
+    if (XFAST) {
+        const uint16_t *p = a.X + (inside ? (int64_t)n * a.ldx + k : 0);
+        const uint4 v = *reinterpret_cast<const uint4 *>(p);
+        return inside ? v : make_uint4(0, 0, 0, 0);
+    }
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (!inside) return v;
+    const uint16_t *p = a.X + (int64_t)n * a.ldx + k;
+    uint16_t h[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) h[j] = (k + j < a.K) ? p[j] : (uint16_t)0;
+    v.x = h[0] | ((uint32_t)h[1] << 16);
+    v.y = h[2] | ((uint32_t)h[3] << 16);
+    v.z = h[4] | ((uint32_t)h[5] << 16);
+    v.w = h[6] | ((uint32_t)h[7] << 16);
+    return v;
+}
+
+// Rounds four consecutive rows m..m+3 of token n to fp16 and stores those < M.
+__device__ inline void store_y4(const SpmmArgs &a, int n, int64_t m, float v0, float v1, float v2, float v3) {
+    const uint16_t h0 = __builtin_bit_cast(uint16_t, (_Float16)v0);
+    const uint16_t h1 = __builtin_bit_cast(uint16_t, (_Float16)v1);
+    const uint16_t h2 = __builtin_bit_cast(uint16_t, (_Float16)v2);
+    const uint16_t h3 = __builtin_bit_cast(uint16_t, (_Float16)v3);
+    uint16_t *dst = a.Y + (int64_t)n * a.ldy + m;
+    if (a.y_vec && m + 4 <= a.M) {
+        *reinterpret_cast<uint2 *>(dst) = make_uint2(h0 | ((uint32_t)h1 << 16), h2 | ((uint32_t)h3 << 16));
+    } else {
+        if (m < a.M) dst[0] = h0;
+        if (m + 1 < a.M) dst[1] = h1;
+        if (m + 2 < a.M) dst[2] = h2;
+        if (m + 3 < a.M) dst[3] = h3;
+    }
+}
+
+// Registers holding one prefetched tile: this lane's share of the X tile and of
+// the wavefront's tile record.
+template <int NT>
+struct TileRegs {
+    uint4 x[2 * NT];
+    uint4 w[8];
+    uint2 msk;
+    int nch;  // 16-byte chunks of packed values (wavefront-uniform)
+};
+
+// Issues the loads of tile (rb, kt) into r: this lane's X chunks, its mask
+// word and the tile's packed values in 1 KB wavefront loads (as many as the
+// record needs; lanes past the record's end read the bytes that follow it,
+// which the device allocation pads, and those chunks are never used). The
+// record offsets come from read-only memory through the scalar path.
+template <int NT, bool XFAST>
+__device__ inline void fetch_tile(const SpmmArgs &a, const uint32_t *__restrict__ off,
+                                  const uint8_t *__restrict__ stream, int64_t rb, bool rb_ok, int64_t kt, int tid,
+                                  int lane, TileRegs<NT> &r) {
+#pragma unroll
+    for (int i = 0; i < 2 * NT; ++i) {
+        const int c = tid + kThreads * i;
+        r.x[i] = load_x_chunk<XFAST>(a, c >> 5, kt * kTileK + 8 * (c & 31));
+    }
+    const int64_t t = (rb_ok ? rb : 0) * a.KT + kt;
+    const uint32_t o0 = off[t], o1 = off[t + 1];
+    const uint8_t *rec = stream + (size_t)o0 * 16;
+    r.msk = reinterpret_cast<const uint2 *>(rec)[lane];  // only used when rb_ok
+    r.nch = rb_ok ? (int)(o1 - o0) - kMaskChunks : 0;
+    const uint4 *vp = reinterpret_cast<const uint4 *>(rec + kMaskBytes);
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+        if (kLanes * i < r.nch) r.w[i] = vp[lane + kLanes * i];
+}
+
+// Workgroup holding unit x when G workgroups split U units evenly: the largest
+// w with floor(w U / G) <= x.
+__device__ inline int64_t unit_owner(int64_t x, int64_t U, int64_t G) { return ((x + 1) * G - 1) / U; }
+
+template <int NT>
+__device__ inline void stage_tile(const TileRegs<NT> &r, uint8_t *xs, uint8_t *region, int tid, int lane) {
+#pragma unroll
+    for (int i = 0; i < 2 * NT; ++i) {
+        const int c = tid + kThreads * i;
+        *reinterpret_cast<uint4 *>(xs + (c >> 5) * kXRowBytes + 16 * (c & 31)) = r.x[i];
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+        if (kLanes * i < r.nch) reinterpret_cast<uint4 *>(region)[lane + kLanes * i] = r.w[i];
+}
+
+template <int NT>
+__device__ inline void compute_tile(uint32_t region, const uint8_t *xs, const uint8_t *lut, uint2 msk, int lane,
+                                    floatx4 (&acc)[NT]) {
+    const StepOffsets so = step_offsets(msk);
+    // Low / high nibble of every mask byte, times 8 (selector table offsets).
+    const uint32_t tlo0 = (msk.x << 3) & 0x78787878u, thi0 = (msk.x >> 1) & 0x78787878u;
+    const uint32_t tlo1 = (msk.y << 3) & 0x78787878u, thi1 = (msk.y >> 1) & 0x78787878u;
+    const uint8_t *xb = xs + (lane & 15) * kXRowBytes + 16 * (lane >> 4);
+    StepWords cur = read_step(region, lut, so, tlo0, thi0, 0);
+#pragma unroll
+    for (int s = 0; s < kSteps; ++s) {
+        StepWords nxt;
+        if (s + 1 < kSteps) nxt = read_step(region, lut, so, s + 1 < 4 ? tlo0 : tlo1, s + 1 < 4 ? thi0 : thi1, s + 1);
+        half8 bv[NT];
+#pragma unroll
+        for (int nb = 0; nb < NT; ++nb) bv[nb] = *reinterpret_cast<const half8 *>(xb + nb * 16 * kXRowBytes + 64 * s);
+        const half8 av = finish_step(cur);
+#pragma unroll
+        for (int nb = 0; nb < NT; ++nb) acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, bv[nb], acc[nb], 0, 0, 0);
+        if (s + 1 < kSteps) cur = nxt;
+    }
+}
+
+// Finishes row group rg for the columns this workgroup accumulated in acc.
+// Lane holds D[4*(lane/16) + i][lane % 16]: rows m0..m0+3 of token 16 nb + lane % 16.
+template <int NT>
+__device__ inline void flush_row_group(const SpmmArgs &a, int64_t rg, int64_t wg, int64_t G, int tid, int lane,
+                                       int wave, const floatx4 (&acc)[NT], uint32_t *last_flag) {
+    const int64_t rb = rg * kWaves + wave;
+    const int64_t m0 = rb * kTileRows + 4 * (lane >> 4);
+    const int64_t w_first = unit_owner(rg * a.KT, a.units, G);
+    const int64_t w_last = unit_owner(rg * a.KT + a.KT - 1, a.units, G);
+    if (w_first == w_last) {  // this workgroup covered every column of the row group
+        if (rb >= a.RB) return;
+#pragma unroll
+        for (int nb = 0; nb < NT; ++nb) {
+            const int n = 16 * nb + (lane & 15);
+            if (n < a.N) store_y4(a, n, m0, acc[nb][0], acc[nb][1], acc[nb][2], acc[nb][3]);
+        }
+        return;
+    }
+    const int64_t nseg = w_last - w_first + 1;
+    // Partials of this row group: [slot][token][64 rows] fp32, accessed through a
+    // buffer resource with device-scope (sc1) cache policy: stores are written
+    // through to the device-coherent level, loads read it.
+    const int64_t slot_floats = (int64_t)a.N * 64;
+    float *slot0 = a.ws + rg * a.maxseg * slot_floats;
+    const __amdgpu_buffer_rsrc_t part =
+        __builtin_amdgcn_make_buffer_rsrc(slot0, (short)0, (int)(nseg * slot_floats * 4), kBufferRsrcWord3);
+    const int mine = (int)((wg - w_first) * slot_floats * 4);
+    const int r0 = wave * kTileRows + 4 * (lane >> 4);  // row within the group
+#pragma unroll
+    for (int nb = 0; nb < NT; ++nb) {
+        const int n = 16 * nb + (lane & 15);
+        if (n >= a.N) continue;
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, acc[nb]), part, mine + (n * 64 + r0) * 4, 0,
+                                               kCachePolicyDevice);
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // every partial store acknowledged before the arrival is counted
+    __syncthreads();
+    if (tid == 0) {
+        const uint32_t old = __hip_atomic_fetch_add(a.cnt + rg, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        *last_flag = (old == (uint32_t)nseg - 1u);
+    }
+    __syncthreads();
+    const bool last = *last_flag != 0;
+    __syncthreads();  // the flag may be reused by the next flush
+    if (!last) return;
+    const int64_t row0 = rg * kWaves * kTileRows;
+    for (int e = tid; e < 16 * a.N; e += kThreads) {  // 4 consecutive rows of one token per item
+        const int n = e >> 4;
+        const int r = 4 * (e & 15);
+        if (row0 + r >= a.RB * kTileRows) continue;
+        floatx4 sum = {0.f, 0.f, 0.f, 0.f};
+        for (int64_t j0 = 0; j0 < nseg; j0 += 8) {
+            // Issue a batch of loads before adding, then add in slot order (fixed order:
+            // bitwise reproducible).
+            v4u32 v[8];
+#pragma unroll
+            for (int jj = 0; jj < 8; ++jj)
+                v[jj] = j0 + jj < nseg ? __builtin_amdgcn_raw_buffer_load_b128(
+                                             part, (int)((j0 + jj) * slot_floats * 4) + (n * 64 + r) * 4, 0,
+                                             kCachePolicyDevice)
+                                       : v4u32{0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int jj = 0; jj < 8; ++jj)
+                if (j0 + jj < nseg) sum += __builtin_bit_cast(floatx4, v[jj]);
+        }
+        store_y4(a, n, row0 + r, sum[0], sum[1], sum[2], sum[3]);
+    }
+    if (tid == 0) __hip_atomic_store(a.cnt + rg, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <int NT, bool XFAST>
+__global__ __launch_bounds__(kThreads, kWgsPerCu) void spmm_kernel(SpmmArgs a, const uint32_t *__restrict__ off,
+                                                                   const uint8_t *__restrict__ stream) {
+    // Wavefront regions first, 8 KB each, so a region offset can be masked; the
+    // last region gets 16 bytes of read slack.
+    __shared__ __attribute__((aligned(kWRegionBytes))) uint8_t wsm[kWaves * kWRegionBytes + 16];
+    __shared__ __attribute__((aligned(16))) uint8_t xs[NT * 16 * kXRowBytes];
+    __shared__ __attribute__((aligned(16))) uint8_t lut[16 * 8];
+    __shared__ uint32_t last_flag;
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    // Wavefront-uniform by construction; saying so lets the tile-offset lookups
+    // be scalar loads, which do not wait on the vector loads in flight.
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t wg = blockIdx.x, G = gridDim.x;
+    const int64_t u0 = wg * a.units / G, u1 = (wg + 1) * a.units / G;
+    if (u0 >= u1) return;
+    uint8_t *region = wsm + wave * kWRegionBytes;
+    if (tid < 16) reinterpret_cast<uint2 *>(lut)[tid] = nibble_selectors((uint32_t)tid);
+
+    floatx4 acc[NT];
+#pragma unroll
+    for (int i = 0; i < NT; ++i) acc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    // One tile in flight: while tile u is decoded from LDS, tile u + 1 is being
+    // loaded into registers. (row group, column tile) advance incrementally.
+    int64_t rg = u0 / a.KT;
+    int64_t kt = u0 % a.KT;
+    TileRegs<NT> buf;
+    fetch_tile<NT, XFAST>(a, off, stream, rg * kWaves + wave, rg * kWaves + wave < a.RB, kt, tid, lane, buf);
+    for (int64_t u = u0; u < u1; ++u) {
+        const int64_t rb = rg * kWaves + wave;
+        int64_t rgn = rg, ktn = kt + 1;
+        if (ktn == a.KT) {
+            ktn = 0;
+            ++rgn;
+        }
+        const bool more = u + 1 < u1;
+        const bool flush_now = !more || ktn == 0;
+        const int64_t rbn = rgn * kWaves + wave;
+        __syncthreads();  // every wavefront is done reading the previous tile
+        stage_tile<NT>(buf, xs, region, tid, lane);
+        const uint2 msk = buf.msk;
+        __syncthreads();
+        if (more && !flush_now) fetch_tile<NT, XFAST>(a, off, stream, rbn, rbn < a.RB, ktn, tid, lane, buf);
+        if (rb < a.RB) compute_tile<NT>(lds_address(region), xs, lut, msk, lane, acc);
+        if (flush_now) {
+            // The flush waits for its own stores; fetching after it keeps that
+            // wait from covering the next tile's loads as well.
+            flush_row_group<NT>(a, rg, wg, G, tid, lane, wave, acc, &last_flag);
+#pragma unroll
+            for (int i = 0; i < NT; ++i) acc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+            if (more) fetch_tile<NT, XFAST>(a, off, stream, rbn, rbn < a.RB, ktn, tid, lane, buf);
+        }
+        rg = rgn;
+        kt = ktn;
+    }
+}
+
+// One wavefront per tile: decode every lane-step and store it densely.
+__global__ __launch_bounds__(64) void densify_kernel(const uint8_t *stream, const uint32_t *off, int64_t M,
+                                                     int64_t K, int64_t KT, uint16_t *Wd, int64_t ldw) {
+    __shared__ __attribute__((aligned(kWRegionBytes))) uint8_t region[kWRegionBytes + 16];
+    __shared__ __attribute__((aligned(16))) uint8_t lut[16 * 8];
+    const int lane = threadIdx.x;
+    const int64_t t = blockIdx.x;
+    const int64_t rb = t / KT, kt = t % KT;
+    if (lane < 16) reinterpret_cast<uint2 *>(lut)[lane] = nibble_selectors((uint32_t)lane);
+    const uint32_t o0 = off[t], o1 = off[t + 1];
+    const uint8_t *rec = stream + (size_t)o0 * 16;
+    const uint2 msk = reinterpret_cast<const uint2 *>(rec)[lane];
+    const int nch = (int)(o1 - o0) - kMaskChunks;
+    const uint4 *vp = reinterpret_cast<const uint4 *>(rec + kMaskBytes);
+    for (int c = lane; c < nch; c += kLanes) reinterpret_cast<uint4 *>(region)[c] = vp[c];
+    __syncthreads();
+    const StepOffsets so = step_offsets(msk);
+    const uint32_t tlo0 = (msk.x << 3) & 0x78787878u, thi0 = (msk.x >> 1) & 0x78787878u;
+    const uint32_t tlo1 = (msk.y << 3) & 0x78787878u, thi1 = (msk.y >> 1) & 0x78787878u;
+    const int64_t row = rb * kTileRows + (lane & 15);
+    if (row >= M) return;
+    for (int s = 0; s < kSteps; ++s) {
+        const half8 av = decode_step(lds_address(region), lut, so, s < 4 ? tlo0 : tlo1, s < 4 ? thi0 : thi1, s);
+        const uint4 u = __builtin_bit_cast(uint4, av);
+        const int64_t col = kt * kTileK + tile_col(lane >> 4, s, 0);
+        uint16_t *dst = Wd + row * ldw + col;
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+        for (int j = 0; j < 8; ++j)
+            if (col + j < K) dst[j] = (uint16_t)(w[j >> 1] >> (16 * (j & 1)));
+    }
+}
+
+}  // namespace
+
+// Workgroups of spmm_kernel<NT, XFAST> resident per CU (queried once per instance).
+template <int NT, bool XFAST>
+static int resident_wgs() {
+    static int cached = 0;
+    if (cached == 0) {
+        int n = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, spmm_kernel<NT, XFAST>, kThreads, 0) != hipSuccess ||
+            n < 1)
+            n = 1;
+        cached = n;
+    }
+    return cached;
+}
+
+static int resident_wgs(int nt, bool xfast) {
+    switch (nt) {
+        case 1: return xfast ? resident_wgs<1, true>() : resident_wgs<1, false>();
+        case 2: return xfast ? resident_wgs<2, true>() : resident_wgs<2, false>();
+        case 3: return xfast ? resident_wgs<3, true>() : resident_wgs<3, false>();
+        default: return xfast ? resident_wgs<4, true>() : resident_wgs<4, false>();
+    }
+}
+
+// Plan of one pass over nt 16-token blocks: the persistent grid fills every CU
+// with as many workgroups as can be resident (at least the slowest variant's
+// count, so the plan does not depend on X's alignment).
+static SpmmPlan plan_pass(const usp_matrix *A, int nt) {
+    SpmmPlan p;
+    p.row_groups = ceil_div(A->RB, kWaves);
+    p.units = p.row_groups * A->KT;
+    const int per_cu = std::min(resident_wgs(nt, true), resident_wgs(nt, false));
+    const int64_t slots = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * per_cu;
+    p.grid = p.units < slots ? p.units : slots;
+    // A range of KT units meets at most ceil(KT / shortest range) + 1 workgroups.
+    const int64_t shortest = p.units / p.grid;
+    p.maxseg = ceil_div(A->KT, shortest) + 1;
+    // Is any row group split over several workgroups?
+    p.split = (p.units % p.grid != 0) || ((p.units / p.grid) % A->KT != 0);
+    return p;
+}
+
+static int pass_nt(int64_t N, int64_t n0) {
+    const int64_t nb = (N - n0) < 16 * kMaxNT ? (N - n0) : 16 * kMaxNT;
+    return (int)((nb + 15) / 16);
+}
+
+SpmmPlan plan_spmm(const usp_matrix *A, int64_t N) { return plan_pass(A, pass_nt(N, 0)); }
+
+// Workspace: one uint32 arrival counter per row group at offset 0 (shared by
+// every pass, zero between passes), padded to 256 bytes, then the fp32 partials
+// of the current pass [row group][slot][tokens][64 rows].
+static size_t counters_bytes(const usp_matrix *A) {
+    return ((size_t)ceil_div(A->RB, kWaves) * sizeof(uint32_t) + 255) / 256 * 256;
+}
+
+static size_t partials_bytes(const SpmmPlan &p, int64_t nb) {
+    return (size_t)p.row_groups * (size_t)p.maxseg * (size_t)nb * 64 * sizeof(float);
+}
+
+size_t spmm_workspace_bytes(const usp_matrix *A, int64_t N) {
+    // Passes run one after another and reuse the workspace: full passes of
+    // 16 * kMaxNT tokens, then one pass over the remainder.
+    size_t need = 0;
+    auto add = [&](int64_t nb) {
+        const SpmmPlan p = plan_pass(A, (int)((nb + 15) / 16));
+        if (p.split) need = std::max(need, partials_bytes(p, nb));
+    };
+    if (N >= 16 * kMaxNT) add(16 * kMaxNT);
+    if (N % (16 * kMaxNT)) add(N % (16 * kMaxNT));
+    return need ? counters_bytes(A) + need : 0;
+}
+
+int launch_spmm(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy, int64_t N,
+                void *workspace, void *stream) {
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    for (int64_t n0 = 0; n0 < N; n0 += 16 * kMaxNT) {
+        const int nb = (int)((N - n0) < 16 * kMaxNT ? (N - n0) : 16 * kMaxNT);
+        const int nt = (nb + 15) / 16;
+        const SpmmPlan p = plan_pass(A, nt);
+        float *ws = p.split ? reinterpret_cast<float *>(reinterpret_cast<uint8_t *>(workspace) + counters_bytes(A))
+                            : nullptr;
+        SpmmArgs a;
+        a.stream = reinterpret_cast<const uint8_t *>(A->d_stream);
+        a.off = A->d_off;
+        a.M = A->M;
+        a.K = A->K;
+        a.RB = A->RB;
+        a.KT = A->KT;
+        a.X = reinterpret_cast<const uint16_t *>(X) + n0 * ldx;
+        a.ldx = ldx;
+        a.Y = reinterpret_cast<uint16_t *>(Y) + n0 * ldy;
+        a.ldy = ldy;
+        a.N = nb;
+        a.units = p.units;
+        a.maxseg = p.maxseg;
+        a.ws = ws;
+        a.cnt = ws ? reinterpret_cast<uint32_t *>(workspace) : nullptr;
+        a.x_vec = ((reinterpret_cast<uintptr_t>(a.X) & 15) == 0) && (ldx % 8 == 0);
+        a.y_vec = ((reinterpret_cast<uintptr_t>(a.Y) & 7) == 0) && (ldy % 4 == 0);
+        const dim3 grid((unsigned)p.grid), block(kThreads);
+        const bool xfast = a.x_vec && (A->K % 8 == 0);
+#define USP_LAUNCH(NTV)                                                                              \
+    if (xfast) hipLaunchKernelGGL((spmm_kernel<NTV, true>), grid, block, 0, st, a, a.off, a.stream); \
+    else hipLaunchKernelGGL((spmm_kernel<NTV, false>), grid, block, 0, st, a, a.off, a.stream);
+        switch (nt) {
+            case 1: USP_LAUNCH(1) break;
+            case 2: USP_LAUNCH(2) break;
+            case 3: USP_LAUNCH(3) break;
+            default: USP_LAUNCH(4) break;
+        }
+#undef USP_LAUNCH
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return (int)e;
+    }
+    return 0;
+}
+
+int launch_densify(const usp_matrix *A, void *Wd, int64_t ldw, void *stream) {
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    const int64_t T = A->RB * A->KT;
+    hipLaunchKernelGGL(densify_kernel, dim3((unsigned)T), dim3(64), 0, st,
+                       reinterpret_cast<const uint8_t *>(A->d_stream), A->d_off, A->M, A->K, A->KT,
+                       reinterpret_cast<uint16_t *>(Wd), ldw);
+    return (int)hipGetLastError();
+}
+
+}  // namespace usp

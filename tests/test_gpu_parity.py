@@ -1,0 +1,201 @@
+"""GPU parity of the sparse product against the CPU oracle, through the C ABI.
+
+Bit-exact where the arithmetic is exact (decode, densify, small-integer
+products, identity columns, zero mask); elsewhere the acceptance bound
+|Y - Yref| <= 1e-2 * (|W||X|) + 1e-3 elementwise and relative Frobenius error
+<= 1e-3, with fp32 accumulation and fp16 output.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    assert t.cuda.is_available()
+    return t
+
+
+@pytest.fixture(scope="module")
+def usp(torch):
+    from paper_2607_08786_amd import usp as mod
+    mod.load_library()
+    return mod
+
+
+def to_dev(torch, bits: np.ndarray):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.float16)).cuda()
+
+
+def run(torch, usp, W, mask, X, ldx_extra=0, offset=0):
+    """Y (N x M float64) from the GPU path; X given as N x K fp16 bits."""
+    A = usp.SparseMatrix(W, mask)
+    N, K = X.shape
+    if ldx_extra or offset:
+        buf = torch.zeros(N * (K + ldx_extra) + offset + 8, dtype=torch.float16, device="cuda")
+        Xv = buf[offset:offset + N * (K + ldx_extra)].view(N, K + ldx_extra)[:, :K]
+        Xv.copy_(to_dev(torch, X))
+    else:
+        Xv = to_dev(torch, X)
+    Y = A.spmm(Xv)
+    torch.cuda.synchronize()
+    A.free()
+    return Y.cpu().numpy().astype(np.float64)
+
+
+def assert_close(Y, W, mask, X, rows=None):
+    Yref, Aref = oracle.masked_gemm(W, mask, X, rows=rows)
+    res = oracle.check_tolerance(Y, Yref, Aref)
+    assert res["ok"], res
+    return res
+
+
+@pytest.mark.parametrize("M,K,N", [(16, 256, 16), (64, 512, 16), (48, 768, 32), (37, 300, 7),
+                                   (128, 1024, 64), (20, 600, 100), (1, 1, 1)])
+def test_small_integers_exact(torch, usp, M, K, N):
+    """Integer W in [-3, 3], X in [-1, 1]: every partial sum and the fp16 output are exact."""
+    W, mask, X = wl.make_small_int(M, K, N, 0.5, seed=1)
+    X = (X.view(np.float16).astype(np.float64).clip(-1, 1)).astype(np.float16).view(np.uint16)
+    Y = run(torch, usp, W, mask, X)
+    Yref, _ = oracle.masked_gemm(W, mask, X)
+    assert np.array_equal(Y, Yref)
+
+
+@pytest.mark.parametrize("M,K", [(16, 256), (64, 1024), (37, 300), (100, 513), (5, 7)])
+def test_densify_bit_exact(torch, usp, M, K):
+    rng = np.random.default_rng(M + K)
+    W = rng.integers(0, 1 << 16, size=(M, K)).astype(np.uint16)
+    mask = (rng.random((M, K)) < 0.5).astype(np.uint8)
+    A = usp.SparseMatrix(W, mask)
+    Wd = A.densify()
+    torch.cuda.synchronize()
+    got = Wd.cpu().numpy().view(np.uint16)
+    A.free()
+    assert np.array_equal(got, oracle.masked_bits(W, mask))
+
+
+def test_decode_roundtrip_through_device(torch, usp):
+    rng = np.random.default_rng(3)
+    W = rng.integers(0, 1 << 16, size=(50, 700)).astype(np.uint16)
+    mask = (rng.random(W.shape) < 0.4).astype(np.uint8)
+    A = usp.SparseMatrix(W, mask)
+    Wo, mo = A.decode()
+    info = A.info()
+    A.free()
+    assert np.array_equal(Wo, oracle.masked_bits(W, mask))
+    assert np.array_equal(mo, mask)
+    assert info["nnz"] == int(mask.sum()) and info["format_version"] == 1
+
+
+def test_tiny_workload_parity(torch, usp):
+    inst = wl.make_instance("tiny", 16)
+    Y = run(torch, usp, inst.W, inst.mask, inst.X)
+    assert_close(Y, inst.W, inst.mask, inst.X)
+
+
+@pytest.mark.parametrize("N", [1, 7, 8, 15, 16, 17, 33, 64, 65, 128, 255, 256])
+def test_n_sweep(torch, usp, N):
+    W, mask, X = wl.make_random(96, 1280, N, 0.5, seed=N)
+    Y = run(torch, usp, W, mask, X)
+    assert_close(Y, W, mask, X)
+
+
+@pytest.mark.parametrize("density", [0.0, 0.3, 0.4, 0.5, 0.6, 0.7, 1.0])
+def test_density_sweep(torch, usp, density):
+    W, mask, X = wl.make_random(80, 2048, 24, density, seed=int(density * 10))
+    Y = run(torch, usp, W, mask, X)
+    if density == 0.0:
+        assert np.all(Y == 0)
+    assert_close(Y, W, mask, X)
+
+
+def test_identity_columns_recover_w(torch, usp):
+    """X = [e_j1 ... e_jN] over every column j: Y reproduces W (masked) exactly."""
+    M, K = 128, 1024
+    W, mask, _ = wl.make_random(M, K, 1, 0.5, seed=11)
+    A = usp.SparseMatrix(W, mask)
+    Wm = oracle.masked_bits(W, mask)
+    for j0 in range(0, K, 256):
+        X = np.zeros((256, K), dtype=np.float16)
+        X[np.arange(256), j0 + np.arange(256)] = 1.0
+        Y = A.spmm(to_dev(torch, X.view(np.uint16)))
+        torch.cuda.synchronize()
+        got = Y.cpu().numpy()  # (256 tokens, M)
+        exp = Wm[:, j0:j0 + 256].view(np.float16).T
+        assert np.array_equal(got.astype(np.float64), exp.astype(np.float64)), j0
+    A.free()
+
+
+def test_deterministic_across_runs(torch, usp):
+    W, mask, X = wl.make_random(320, 5120, 16, 0.5, seed=2)
+    A = usp.SparseMatrix(W, mask)
+    Xd = to_dev(torch, X)
+    Y1 = A.spmm(Xd).clone()
+    Y2 = A.spmm(Xd).clone()
+    torch.cuda.synchronize()
+    A.free()
+    assert torch.equal(Y1.view(torch.int16), Y2.view(torch.int16))
+
+
+def test_strided_and_unaligned_x(torch, usp):
+    W, mask, X = wl.make_random(64, 777, 9, 0.5, seed=4)
+    Y = run(torch, usp, W, mask, X, ldx_extra=3, offset=1)
+    assert_close(Y, W, mask, X)
+
+
+def test_special_values_follow_ieee(torch, usp):
+    M, K, N = 16, 256, 16
+    W, mask, X = wl.make_small_int(M, K, N, 0.5, seed=5)
+    W = W.copy()
+    mask = mask.copy()
+    W[0, 3], mask[0, 3] = 0x7C00, 1  # +Inf kept
+    W[1, 5], mask[1, 5] = 0x7E00, 1  # NaN kept
+    W[2, 9], mask[2, 9] = 0x7C00, 0  # Inf pruned: no effect
+    W[3, 0], mask[3, 0] = 0x0001, 1  # smallest subnormal kept
+    Y = run(torch, usp, W, mask, X)
+    Yref, _ = oracle.masked_gemm(W, mask, X)
+    assert np.array_equal(np.isnan(Y), np.isnan(Yref))
+    fin = ~np.isnan(Yref)
+    assert np.array_equal(np.isinf(Y[fin]), np.isinf(Yref[fin]))
+    ok = np.isfinite(Yref)
+    assert np.allclose(Y[ok], Yref[ok], rtol=1e-2, atol=1e-3)
+
+
+def test_zero_mask_gives_exact_zero(torch, usp):
+    W, _, X = wl.make_random(64, 512, 16, 0.5, seed=6)
+    Y = run(torch, usp, W, np.zeros(W.shape, np.uint8), X)
+    assert np.all(Y == 0)
+
+
+def test_workspace_contract(torch, usp):
+    W, mask, X = wl.make_random(64, 4096, 16, 0.5, seed=7)
+    A = usp.SparseMatrix(W, mask)
+    need = A.workspace_size(16)
+    if need:
+        with pytest.raises(usp.UspError):
+            usp.usp_spmm(A.handle, to_dev(torch, X), torch.empty((16, 64), dtype=torch.float16, device="cuda"),
+                         None)
+    A.free()
+
+
+# Full-size workloads, sampled output rows (the oracle computes them one by one),
+# in the same launch configuration the benchmark times.
+@pytest.mark.parametrize("name,N,s", [("attn13b", 16, 50), ("attn13b", 8, 50), ("ffn13b_up", 64, 50),
+                                      ("ffn13b_down", 16, 50), ("ffn70b", 16, 50), ("ffn70b", 256, 40),
+                                      ("ffn70b", 32, 70), ("ffn66b", 16, 60)])
+def test_workload_sampled_rows(torch, usp, name, N, s):
+    inst = wl.make_instance(name, N, s)
+    A = usp.SparseMatrix(inst.W, inst.mask)
+    Y = A.spmm(to_dev(torch, inst.X))
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(0)
+    rows = np.sort(np.unique(np.concatenate([rng.choice(inst.M, 192, replace=False),
+                                             [0, 15, 16, inst.M - 1]])))
+    got = Y.cpu().numpy().astype(np.float64)[:, rows]
+    A.free()
+    assert_close(got, inst.W, inst.mask, inst.X, rows=rows)

@@ -11,10 +11,11 @@ product Y is M x N. Storage conventions used throughout this repository:
   K x N matrix (the ``[B, H]`` activation of Section 2.1), fp16 bit patterns.
 
 Every draw comes from ``numpy.random.default_rng(SeedSequence([2607, cfg_id,
-stream, n_or_0]))`` with stream 0 = W values, 1 = mask / column scales,
-2 = X. Samples are drawn in float64 and cast to fp16 with round-to-nearest-even.
-Row draws are taken in fixed chunks of ``ROW_CHUNK`` rows so that memory stays
-bounded; the chunking is part of the definition of each instance.
+stream, n_or_0, chunk]))`` with stream 0 = W values, 1 = mask / column scales,
+2 = X, and ``chunk`` the index of a block of ``ROW_CHUNK`` rows (0 for draws
+that are not chunked). Chunks are independent streams, so they are drawn in
+parallel threads. W samples are drawn in float32 and cast to fp16 with
+round-to-nearest-even; X in float64.
 
 Pruning is magnitude based (Section 5.3 prunes with Wanda; real weights are not
 available here, so magnitudes of synthetic weights stand in):
@@ -27,17 +28,32 @@ available here, so magnitudes of synthetic weights stand in):
 """
 from __future__ import annotations
 
+import concurrent.futures
 import dataclasses
 import hashlib
+import os
 
 import numpy as np
 
 ROW_CHUNK = 1024
 BASE_SEED = 2607
+_WORKERS = max(1, min(16, os.cpu_count() or 1))
 
 
-def seed_for(cfg_id: int, stream: int, n_or_0: int = 0) -> np.random.Generator:
-    return np.random.default_rng(np.random.SeedSequence([BASE_SEED, cfg_id, stream, n_or_0]))
+def seed_for(cfg_id: int, stream: int, n_or_0: int = 0, chunk: int = 0) -> np.random.Generator:
+    return np.random.default_rng(np.random.SeedSequence([BASE_SEED, cfg_id, stream, n_or_0, chunk]))
+
+
+def _parallel_chunks(M: int, fn) -> None:
+    """Calls fn(chunk_index, r0, r1) for every ROW_CHUNK block of rows, in threads."""
+    blocks = [(c, r0, min(M, r0 + ROW_CHUNK)) for c, r0 in enumerate(range(0, M, ROW_CHUNK))]
+    if len(blocks) == 1 or _WORKERS == 1:
+        for b in blocks:
+            fn(*b)
+        return
+    with concurrent.futures.ThreadPoolExecutor(_WORKERS) as ex:
+        for f in [ex.submit(fn, *b) for b in blocks]:
+            f.result()
 
 
 def keep_count(K: int, sparsity_pct: int) -> int:
@@ -50,18 +66,26 @@ def _f16_bits(a: np.ndarray) -> np.ndarray:
 
 
 def draw_weights(cfg_id: int, M: int, K: int, dist: str, scale: float) -> np.ndarray:
-    """M x K fp16 bit patterns, drawn ROW_CHUNK rows at a time."""
-    rng = seed_for(cfg_id, 0)
+    """M x K fp16 bit patterns; chunk c of ROW_CHUNK rows uses its own seed.
+
+    normal: scale * Z; student_t4: scale * Z / sqrt(G / 2) with G ~ Gamma(2, 1),
+    i.e. Z over the root of a chi-square(4) variable divided by its 4 degrees
+    of freedom (Student's t with 4 degrees of freedom).
+    """
+    if dist not in ("normal", "student_t4"):
+        raise ValueError(dist)
     out = np.empty((M, K), dtype=np.uint16)
-    for r0 in range(0, M, ROW_CHUNK):
-        r1 = min(M, r0 + ROW_CHUNK)
-        if dist == "normal":
-            v = rng.normal(0.0, scale, size=(r1 - r0, K))
-        elif dist == "student_t4":
-            v = rng.standard_t(4, size=(r1 - r0, K)) * scale
-        else:
-            raise ValueError(dist)
-        out[r0:r1] = _f16_bits(v)
+
+    def fill(c, r0, r1):
+        rng = seed_for(cfg_id, 0, 0, c)
+        z = rng.standard_normal((r1 - r0, K), dtype=np.float32)
+        if dist == "student_t4":
+            g = rng.standard_gamma(2.0, size=(r1 - r0, K), dtype=np.float32)
+            z /= np.sqrt(g * np.float32(0.5))
+        z *= np.float32(scale)
+        out[r0:r1] = z.astype(np.float16).view(np.uint16)
+
+    _parallel_chunks(M, fill)
     return out
 
 
@@ -84,42 +108,54 @@ def prune_per_row(score: np.ndarray, keep: int) -> np.ndarray:
     if keep >= K:
         mask[:] = 1
         return mask
-    for r0 in range(0, M, ROW_CHUNK):
-        s = score[r0:r0 + ROW_CHUNK]
-        srt = np.sort(s, axis=1)
-        t = srt[:, K - keep][:, None]
+
+    def fill(c, r0, r1):
+        s = score[r0:r1]
+        t = np.partition(s, K - keep, axis=1)[:, K - keep][:, None]  # keep-th largest
         gt = s > t
         eq = s == t
         need = keep - gt.sum(axis=1, keepdims=True)
         take_eq = eq & (np.cumsum(eq, axis=1) <= need)
-        mask[r0:r0 + ROW_CHUNK] = gt | take_eq
+        mask[r0:r1] = gt | take_eq
+
+    _parallel_chunks(M, fill)
     return mask
 
 
 def prune_global(W: np.ndarray, keep: int) -> np.ndarray:
     """Keep the ``keep`` largest |w| of the whole matrix (ties: lower row-major index)."""
     M, K = W.shape
-    mag = _magnitude_bits(W)
-    hist = np.bincount(mag.ravel(), minlength=1 << 15).astype(np.int64)
-    # number of entries with magnitude >= t, for every t
-    ge = np.cumsum(hist[::-1])[::-1]
-    # threshold bin t: count(mag > t) < keep <= count(mag >= t)
-    t = int(np.nonzero(ge >= keep)[0].max()) if keep > 0 else (1 << 15)
     mask = np.zeros((M, K), dtype=np.uint8)
     if keep <= 0:
         return mask
+    hists = [None] * ((M + ROW_CHUNK - 1) // ROW_CHUNK)
+
+    def hist(c, r0, r1):
+        hists[c] = np.bincount(_magnitude_bits(W[r0:r1]).ravel(), minlength=1 << 15)
+
+    _parallel_chunks(M, hist)
+    h = np.sum(hists, axis=0).astype(np.int64)
+    ge = np.cumsum(h[::-1])[::-1]  # ge[t] = count(|w| bits >= t)
+    t = int(np.nonzero(ge >= keep)[0].max())
     n_gt = int(ge[t + 1]) if t + 1 < len(ge) else 0
-    need = keep - n_gt
-    taken = 0
-    for r0 in range(0, M, ROW_CHUNK):
-        m = mag[r0:r0 + ROW_CHUNK]
-        gt = m > t
-        eq = m == t
-        flat_eq = eq.ravel()
-        c = np.cumsum(flat_eq) + taken
-        take = (flat_eq & (c <= need)).reshape(eq.shape)
-        taken = min(need, taken + int(flat_eq.sum()))
-        mask[r0:r0 + ROW_CHUNK] = gt | take
+    need = keep - n_gt  # entries with magnitude bits == t to keep, lowest index first
+    eq_counts = [0] * len(hists)
+
+    def above(c, r0, r1):
+        m = _magnitude_bits(W[r0:r1])
+        mask[r0:r1] = m > t
+        eq_counts[c] = int(np.count_nonzero(m == t))
+
+    _parallel_chunks(M, above)
+    for c, r0 in enumerate(range(0, M, ROW_CHUNK)):
+        if need <= 0:
+            break
+        if eq_counts[c] == 0:
+            continue
+        r1 = min(M, r0 + ROW_CHUNK)
+        idx = np.flatnonzero(_magnitude_bits(W[r0:r1]) == t)[:need]
+        mask[r0:r1].reshape(-1)[idx] = 1
+        need -= idx.size
     return mask
 
 
