@@ -46,7 +46,9 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-dense", action="store_true", help="skip the hipBLASLt dense baseline")
-    ap.add_argument("--sweep", action="store_true", help="also time every instance of the workload (extra lines)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run an untimed 256 MiB device copy: the reference kernel that scales "
+                         "rocprofv3 FETCH_SIZE / WRITE_SIZE readings to bytes")
     return ap.parse_args()
 
 
@@ -92,14 +94,17 @@ def cpu_baseline(inst, seconds):
     probe = np.sort(rng.choice(inst.M, min(inst.M, 32), replace=False))
     oracle.masked_gemm(inst.W, inst.mask, inst.X, rows=probe, lib=lib)
     per_row = (time.perf_counter() - t0) / probe.size
-    rows_n = int(max(1, min(inst.M, seconds / max(per_row, 1e-9))))
+    want = seconds / max(per_row, 1e-9)  # rows that take about `seconds`
+    rows_n = int(max(1, min(inst.M, want)))
+    reps = int(max(1, min(100, want // inst.M)))  # small layers: repeat the whole product
     rows = np.sort(rng.choice(inst.M, rows_n, replace=False))
     t0 = time.perf_counter()
-    oracle.masked_gemm(inst.W, inst.mask, inst.X, rows=rows, lib=lib)
+    for _ in range(reps):
+        oracle.masked_gemm(inst.W, inst.mask, inst.X, rows=rows, lib=lib)
     dt = time.perf_counter() - t0
-    flops = 2.0 * rows_n * inst.K * inst.N  # dense-equivalent, like the metric
+    flops = 2.0 * reps * rows_n * inst.K * inst.N  # dense-equivalent, like the metric
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(lib), "kind": "oracle",
-            "sample": f"{rows_n} of {inst.M} output rows (all K={inst.K}, N={inst.N}), {dt:.1f} s, float64"}
+            "sample": f"{reps} x {rows_n} of {inst.M} output rows (all K={inst.K}, N={inst.N}), {dt:.1f} s, float64"}
 
 
 def traffic_record(kernel_digest):
@@ -195,6 +200,13 @@ def main():
     if dense is not None:
         out["dense_hipblaslt"] = dense
         out["speedup_vs_hipblaslt"] = dense["ms_per_call"] / ms
+    if args.calibrate_copy:
+        src = torch.empty(256 * 2**20, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        out["calibration_copy_bytes"] = src.numel()
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(inst, args.cpu_seconds)
     print(json.dumps(out), flush=True)
