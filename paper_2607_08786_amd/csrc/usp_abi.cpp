@@ -73,6 +73,7 @@ usp_status usp_encode(const uint16_t *W, int64_t ldw, const uint8_t *mask, int64
     A->RB = enc.RB;
     A->KT = enc.KT;
     A->nnz = enc.nnz;
+    A->max_chunks = enc.max_chunks;
     A->stream_bytes = enc.stream.size();
     A->d_stream = nullptr;
     A->d_off = nullptr;

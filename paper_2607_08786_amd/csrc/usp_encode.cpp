@@ -69,15 +69,18 @@ void encode_host(const uint16_t *W, int64_t ldw, const uint8_t *mask, int64_t ld
         }
     });
     out.off.assign(T + 1, 0);
-    int64_t total = 0, nnz = 0;
+    int64_t total = 0, nnz = 0, max_chunks = 0;
     for (int64_t t = 0; t < T; ++t) {
         out.off[t] = (uint32_t)total;
-        total += kMaskChunks + ceil_div(2 * tile_nnz[t], 16);
+        const int64_t chunks = ceil_div(2 * tile_nnz[t], 16);
+        total += kMaskChunks + chunks;
+        max_chunks = std::max(max_chunks, chunks);
         nnz += tile_nnz[t];
         if (total >= (int64_t(1) << 32)) throw std::bad_alloc();
     }
     out.off[T] = (uint32_t)total;
     out.nnz = nnz;
+    out.max_chunks = max_chunks;
     out.stream.assign((size_t)total * 16, 0);
 
     // Pass 2: fill records.

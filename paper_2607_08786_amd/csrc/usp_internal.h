@@ -15,6 +15,7 @@ struct usp_matrix {
     int64_t M, K;            // logical shape
     int64_t RB, KT;          // row blocks (16 rows) and column tiles (256 columns)
     int64_t nnz;
+    int64_t max_chunks;      // most 16-byte value chunks in one tile record
     size_t stream_bytes;     // bytes of all tile records
     void *d_stream;          // device: tile records
     uint32_t *d_off;         // device: RB*KT + 1 offsets in 16-byte units
@@ -28,6 +29,7 @@ constexpr uint32_t kMagic = 0x55535031u;  // "USP1"
 // Host-side encoding result (before upload).
 struct HostEncoding {
     int64_t M = 0, K = 0, RB = 0, KT = 0, nnz = 0;
+    int64_t max_chunks = 0;        // most 16-byte value chunks in one record
     std::vector<uint32_t> off;     // RB*KT + 1 entries, 16-byte units
     std::vector<uint8_t> stream;   // 16 * off.back() bytes
 };

@@ -102,16 +102,18 @@ struct StepWords {
 
 typedef const __attribute__((address_space(3))) uint32_t lds_u32;
 
-// Byte address of an LDS object (LDS addresses are 32-bit).
-__device__ inline uint32_t lds_address(const void *p) {
-    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+// An LDS array seen as 32-bit words. Indexing the array itself (rather than an
+// integer address) lets the compiler tell LDS arrays apart, which its waits for
+// direct-to-LDS loads rely on.
+__device__ inline lds_u32 *as_lds(const void *p) {
+    return (lds_u32 *)(const __attribute__((address_space(3))) void *)p;
 }
 
-// region_base: LDS address of the wavefront's 8 KB-aligned region, so adding
-// the masked offset is a single OR.
-__device__ inline void read_nibble(uint32_t region_base, uint32_t hb, uint32_t idx8, const uint8_t *lut,
+// region: the staged values. The byte offset is bounded by the largest record
+// (8 KB), so a read never leaves the region's neighbourhood.
+__device__ inline void read_nibble(lds_u32 *region, uint32_t hb, uint32_t idx8, const uint8_t *lut,
                                    uint32_t *e, uint2 &sel) {
-    lds_u32 *d = (lds_u32 *)(uintptr_t)((hb & (kWRegionBytes - 4)) | region_base);
+    lds_u32 *d = region + ((hb & (kWRegionBytes - 4)) >> 2);
     e[0] = d[0];
     e[1] = d[1];
     e[2] = d[2];
@@ -182,7 +184,7 @@ __device__ inline StepOffsets step_offsets(uint2 msk) {
 
 // Issues the LDS reads of step s of the staged tile.
 // tlo/thi: mask bytes of the step's low / high nibbles pre-scaled by 8.
-__device__ inline StepWords read_step(uint32_t region, const uint8_t *lut, const StepOffsets &so,
+__device__ inline StepWords read_step(lds_u32 *region, const uint8_t *lut, const StepOffsets &so,
                                       uint32_t tlo, uint32_t thi, int s) {
     StepWords w;
     const uint32_t P = (so.excl[s / 3] >> (10 * (s % 3))) & 0x3FFu;
@@ -203,7 +205,7 @@ __device__ inline half8 finish_step(const StepWords &w) {
     return __builtin_bit_cast(half8, a);
 }
 
-__device__ inline half8 decode_step(uint32_t region, const uint8_t *lut, const StepOffsets &so,
+__device__ inline half8 decode_step(lds_u32 *region, const uint8_t *lut, const StepOffsets &so,
                                     uint32_t tlo, uint32_t thi, int s) {
     return finish_step(read_step(region, lut, so, tlo, thi, s));
 }
@@ -303,7 +305,7 @@ __device__ inline void stage_tile(const TileRegs<NT> &r, uint8_t *xs, uint8_t *r
 }
 
 template <int NT>
-__device__ inline void compute_tile(uint32_t region, const uint8_t *xs, const uint8_t *lut, uint2 msk, int lane,
+__device__ inline void compute_tile(lds_u32 *region, const uint8_t *xs, const uint8_t *lut, uint2 msk, int lane,
                                     floatx4 (&acc)[NT]) {
     const StepOffsets so = step_offsets(msk);
     // Low / high nibble of every mask byte, times 8 (selector table offsets).
@@ -396,7 +398,7 @@ __device__ inline void flush_row_group(const SpmmArgs &a, int64_t rg, int64_t wg
 }
 
 template <int NT, bool XFAST>
-__global__ __launch_bounds__(kThreads, kWgsPerCu) void spmm_kernel(SpmmArgs a, const uint32_t *__restrict__ off,
+__global__ __launch_bounds__(kThreads, 2) void spmm_kernel(SpmmArgs a, const uint32_t *__restrict__ off,
                                                                    const uint8_t *__restrict__ stream) {
     // Wavefront regions first, 8 KB each, so a region offset can be masked; the
     // last region gets 16 bytes of read slack.
@@ -440,7 +442,7 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void spmm_kernel(SpmmArgs a, c
         const uint2 msk = buf.msk;
         __syncthreads();
         if (more && !flush_now) fetch_tile<NT, XFAST>(a, off, stream, rbn, rbn < a.RB, ktn, tid, lane, buf);
-        if (rb < a.RB) compute_tile<NT>(lds_address(region), xs, lut, msk, lane, acc);
+        if (rb < a.RB) compute_tile<NT>(as_lds(region), xs, lut, msk, lane, acc);
         if (flush_now) {
             // The flush waits for its own stores; fetching after it keeps that
             // wait from covering the next tile's loads as well.
@@ -452,6 +454,443 @@ __global__ __launch_bounds__(kThreads, kWgsPerCu) void spmm_kernel(SpmmArgs a, c
         rg = rgn;
         kt = ktn;
     }
+}
+
+// ---------------------------------------------------------------------------
+// Barrier-free streaming kernel for up to 16 tokens.
+//
+// Every wavefront is its own workgroup and streams its own contiguous range of
+// units with no workgroup barrier: coupling four wavefronts with barriers made
+// each tile wait for the slowest of four loads and halved the achievable HBM
+// rate. A unit is (row set, column tile): R row blocks that share one column
+// tile, so the wavefront loads the tile's MFMA B operands (X, 16 bytes per lane
+// and step) once for R records; X stays resident in L2. One record is in
+// flight: the next record is loaded while the current one is decoded, so only
+// the R accumulators grow with R.
+// All loads go through buffer resources (SGPR base, constant lane offsets,
+// hardware zero-fill out of range). A record is read with L 1 KB loads, L
+// being the smallest count that covers every record of the matrix; the
+// resource ends at the record's own end, so the loads past it fetch nothing.
+// The count per unit is fixed, so the compiler's waits are exact.
+// A row set split over several wavefronts is finished by the last to arrive; a
+// wavefront stores its partial at the end of its segment and counts its arrival
+// at its next unit boundary, where it waits for its loads anyway.
+// ---------------------------------------------------------------------------
+
+struct WaveArgs {
+    int64_t M, K, RB, KT;
+    int64_t sets, units, maxseg;  // row sets; sets * KT; partial slots per row set
+    const uint16_t *X;
+    int64_t ldx;
+    uint32_t x_bytes;             // readable bytes of X from its base
+    uint16_t *Y;
+    int64_t ldy;
+    int N;
+    float *ws;                    // partials [set][slot][token][16 R rows], or null
+    uint32_t *cnt;                // arrival counters per row set (zero between calls)
+    int y_vec;
+};
+
+// Rows m..m+3 of token n (a lane's MFMA outputs), rounded to fp16, those < M.
+__device__ inline void store_rows4(const WaveArgs &a, int n, int64_t m, const floatx4 &v) {
+    const uint16_t h0 = __builtin_bit_cast(uint16_t, (_Float16)v[0]);
+    const uint16_t h1 = __builtin_bit_cast(uint16_t, (_Float16)v[1]);
+    const uint16_t h2 = __builtin_bit_cast(uint16_t, (_Float16)v[2]);
+    const uint16_t h3 = __builtin_bit_cast(uint16_t, (_Float16)v[3]);
+    uint16_t *dst = a.Y + (int64_t)n * a.ldy + m;
+    if (a.y_vec && m + 4 <= a.M) {
+        *reinterpret_cast<uint2 *>(dst) = make_uint2(h0 | ((uint32_t)h1 << 16), h2 | ((uint32_t)h3 << 16));
+    } else {
+        if (m < a.M) dst[0] = h0;
+        if (m + 1 < a.M) dst[1] = h1;
+        if (m + 2 < a.M) dst[2] = h2;
+        if (m + 3 < a.M) dst[3] = h3;
+    }
+}
+
+// Counts this wavefront's arrival at row set `set` (its partial must already be
+// acknowledged); returns the counter's previous value (in lane 0).
+__device__ inline uint32_t arrive_count(const WaveArgs &a, int64_t set, int lane) {
+    uint32_t old = 0;
+    if (lane == 0) old = __hip_atomic_fetch_add(a.cnt + set, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return old;
+}
+
+// With the counter's previous value: the last of the nseg arrivals sums every
+// slot in order, stores Y and resets the counter.
+template <int R>
+__device__ inline void arrive_finish(const WaveArgs &a, int64_t set, int64_t nseg, uint32_t old, int lane) {
+    old = __builtin_amdgcn_readfirstlane(old);
+    if (old != (uint32_t)nseg - 1u) return;
+    const int64_t slot_floats = (int64_t)a.N * kTileRows * R;
+    float *slot0 = a.ws + set * a.maxseg * slot_floats;
+    const __amdgpu_buffer_rsrc_t part =
+        __builtin_amdgcn_make_buffer_rsrc(slot0, (short)0, (int)(nseg * slot_floats * 4), kBufferRsrcWord3);
+    const int n = lane & 15, g4 = 4 * (lane >> 4);
+    if (n < a.N) {
+#pragma unroll 1
+        for (int r = 0; r < R; ++r) {  // not unrolled: keeps this rare path's registers few
+            const int lofs = (n * kTileRows * R + kTileRows * r + g4) * 4;
+            floatx4 sum = {0.f, 0.f, 0.f, 0.f};
+            for (int64_t j0 = 0; j0 < nseg; j0 += 8) {
+                v4u32 v[8];
+#pragma unroll
+                for (int jj = 0; jj < 8; ++jj)  // a batch of loads, then adds in slot order
+                    v[jj] = j0 + jj < nseg ? __builtin_amdgcn_raw_buffer_load_b128(
+                                                 part, (int)((j0 + jj) * slot_floats * 4) + lofs, 0, kCachePolicyDevice)
+                                           : v4u32{0u, 0u, 0u, 0u};
+#pragma unroll
+                for (int jj = 0; jj < 8; ++jj)
+                    if (j0 + jj < nseg) sum += __builtin_bit_cast(floatx4, v[jj]);
+            }
+            store_rows4(a, n, (set * R + r) * kTileRows + g4, sum);
+        }
+    }
+    if (lane == 0) __hip_atomic_store(a.cnt + set, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <int R>
+__device__ inline void arrive_row_set(const WaveArgs &a, int64_t set, int64_t nseg, int lane) {
+    arrive_finish<R>(a, set, nseg, arrive_count(a, set, lane), lane);
+}
+
+// One tile record in registers: this lane's mask word and L KB of the packed
+// values (16 bytes per lane per load).
+template <int L>
+struct WaveRec {
+    v4u32 w[L];
+    uint2 msk;
+};
+
+// Loads record (rb, kt); a row block past the matrix (the missing half of the
+// last row set) gets an empty resource, so its mask and values read as zero.
+template <int L>
+__device__ inline void fetch_rec(const WaveArgs &a, const uint32_t *__restrict__ off,
+                                 const uint8_t *__restrict__ stream, int64_t rb, int64_t kt, int lane,
+                                 WaveRec<L> &r) {
+    uint32_t o0 = 0, o1 = 0;
+    if (rb < a.RB) {
+        const int64_t t = rb * a.KT + kt;
+        o0 = off[t];
+        o1 = off[t + 1];
+    }
+    const __amdgpu_buffer_rsrc_t rec = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(stream + (uint64_t)o0 * 16), (short)0, (int)((o1 - o0) * 16), kBufferRsrcWord3);
+    r.msk = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rec, lane * 8, 0, 0));
+#pragma unroll
+    for (int i = 0; i < L; ++i)
+        r.w[i] = __builtin_amdgcn_raw_buffer_load_b128(rec, kMaskBytes + 1024 * i + lane * 16, 0, 0);
+}
+
+// B operands of one tile: step s, lane (g = lane / 16, n = lane % 16) holds
+// X[n][256 kt + 32 s + 8 g .. + 7]; zero for n >= N (out of the X resource) and
+// for columns >= K.
+__device__ inline void fetch_x(const WaveArgs &a, __amdgpu_buffer_rsrc_t xr, int xoff, int64_t kt, int lane,
+                               v4u32 (&xb)[kSteps]) {
+    const int base = xoff + (int)(kt * kTileK * 2);
+#pragma unroll
+    for (int s = 0; s < kSteps; ++s) xb[s] = __builtin_amdgcn_raw_buffer_load_b128(xr, base + 64 * s, 0, 0);
+    if ((kt + 1) * kTileK > a.K) {  // last, partial column tile
+#pragma unroll
+        for (int s = 0; s < kSteps; ++s)
+            if (kt * kTileK + 32 * s + 8 * (lane >> 4) >= a.K) xb[s] = v4u32{0u, 0u, 0u, 0u};
+    }
+}
+
+// R row blocks per unit, L KB of record values per load group.
+template <int R, int L>
+__global__ __launch_bounds__(kLanes) void spmm_wave_kernel(WaveArgs a, const uint32_t *__restrict__ off,
+                                                          const uint8_t *__restrict__ stream) {
+    constexpr int kRegion = 1024 * L + 16;  // staged values + the decode's 12-byte overread
+    __shared__ __attribute__((aligned(16))) uint8_t region[kRegion];
+    __shared__ __attribute__((aligned(16))) uint8_t lut[16 * 8];
+    const int lane = threadIdx.x;
+    const int64_t w = blockIdx.x, G = gridDim.x;
+    const int64_t u0 = w * a.units / G, u1 = (w + 1) * a.units / G;
+    if (u0 >= u1) return;
+    if (lane < 16) reinterpret_cast<uint2 *>(lut)[lane] = nibble_selectors((uint32_t)lane);
+    lds_u32 *const rbase = as_lds(region);
+
+    const __amdgpu_buffer_rsrc_t xr =
+        __builtin_amdgcn_make_buffer_rsrc((void *)a.X, (short)0, (int)a.x_bytes, kBufferRsrcWord3);
+    const int n_lane = lane & 15, g4 = 4 * (lane >> 4);
+    // Lanes of tokens >= N start at the resource's end: every load they issue is
+    // out of range and returns zeros.
+    const int xoff = n_lane < a.N ? (int)(n_lane * a.ldx * 2) + 16 * (lane >> 4) : (int)a.x_bytes;
+
+    floatx4 acc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) acc[r] = floatx4{0.f, 0.f, 0.f, 0.f};
+    int64_t set = u0 / a.KT, kt = u0 % a.KT;
+    int64_t pend_set = -1, pend_nseg = 0;  // partial stored, arrival not yet counted
+    // One record in flight: record r + 1 (or the next unit's first) is loaded
+    // while record r is decoded.
+    WaveRec<L> cur;
+    fetch_rec<L>(a, off, stream, set * R, kt, lane, cur);
+    for (int64_t u = u0; u < u1; ++u) {
+        int64_t setn = set, ktn = kt + 1;
+        if (ktn == a.KT) {
+            ktn = 0;
+            ++setn;
+        }
+        const bool more = u + 1 < u1;
+        v4u32 xb[kSteps];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            // Stage the record (in-order LDS: the previous decode's reads are done).
+#pragma unroll
+            for (int i = 0; i < L; ++i) reinterpret_cast<v4u32 *>(region)[lane + kLanes * i] = cur.w[i];
+            const uint2 msk = cur.msk;
+            if (r == 0) {
+                if (pend_set >= 0) {  // the partial's stores completed with the record's loads
+                    __builtin_amdgcn_s_waitcnt(0);
+                    arrive_row_set<R>(a, pend_set, pend_nseg, lane);
+                    pend_set = -1;
+                }
+                fetch_x(a, xr, xoff, kt, lane, xb);
+            }
+            // Next record (past the range's end: this unit's first again, unused).
+            if (r + 1 < R) fetch_rec<L>(a, off, stream, set * R + r + 1, kt, lane, cur);
+            else fetch_rec<L>(a, off, stream, (more ? setn : set) * R, more ? ktn : kt, lane, cur);
+
+            const StepOffsets so = step_offsets(msk);
+            const uint32_t tlo0 = (msk.x << 3) & 0x78787878u, thi0 = (msk.x >> 1) & 0x78787878u;
+            const uint32_t tlo1 = (msk.y << 3) & 0x78787878u, thi1 = (msk.y >> 1) & 0x78787878u;
+            StepWords sw = read_step(rbase, lut, so, tlo0, thi0, 0);
+#pragma unroll
+            for (int s = 0; s < kSteps; ++s) {
+                StepWords nx;
+                if (s + 1 < kSteps)
+                    nx = read_step(rbase, lut, so, s + 1 < 4 ? tlo0 : tlo1, s + 1 < 4 ? thi0 : thi1, s + 1);
+                const half8 av = finish_step(sw);
+                acc[r] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, __builtin_bit_cast(half8, xb[s]), acc[r], 0, 0, 0);
+                if (s + 1 < kSteps) sw = nx;
+            }
+        }
+
+        if (!more || ktn == 0) {  // end of this wavefront's segment of the row set
+            const int64_t w_first = unit_owner(set * a.KT, a.units, G);
+            const int64_t w_last = unit_owner(set * a.KT + a.KT - 1, a.units, G);
+            if (w_first == w_last) {
+                if (n_lane < a.N) {
+#pragma unroll
+                    for (int r = 0; r < R; ++r) store_rows4(a, n_lane, (set * R + r) * kTileRows + g4, acc[r]);
+                }
+            } else {
+                const int64_t slot_floats = (int64_t)a.N * kTileRows * R;
+                float *slot = a.ws + (set * a.maxseg + (w - w_first)) * slot_floats;
+                const __amdgpu_buffer_rsrc_t part =
+                    __builtin_amdgcn_make_buffer_rsrc(slot, (short)0, (int)(slot_floats * 4), kBufferRsrcWord3);
+                if (n_lane < a.N) {
+#pragma unroll
+                    for (int r = 0; r < R; ++r)
+                        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, acc[r]), part,
+                                                               (n_lane * kTileRows * R + kTileRows * r + g4) * 4, 0,
+                                                               kCachePolicyDevice);
+                }
+                pend_set = set;
+                pend_nseg = w_last - w_first + 1;
+            }
+#pragma unroll
+            for (int r = 0; r < R; ++r) acc[r] = floatx4{0.f, 0.f, 0.f, 0.f};
+        }
+        set = setn;
+        kt = ktn;
+    }
+    if (pend_set >= 0) {
+        __builtin_amdgcn_s_waitcnt(0);
+        arrive_row_set<R>(a, pend_set, pend_nseg, lane);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Direct-to-LDS variant of the wave kernel (4 row blocks per unit).
+//
+// Records are loaded by buffer-to-LDS transfers into a ring of four LDS slots,
+// one per row block of the unit, so three records are in flight while one is
+// decoded and no VGPRs hold them. Each slot is its own LDS array: the compiler
+// waits for exactly the transfers into the slot a decode reads. The unit's X
+// operands are loaded into registers one unit ahead.
+// ---------------------------------------------------------------------------
+
+constexpr int kDmaRows = 4;  // row blocks per unit = LDS slots
+
+// Encoding of s_waitcnt that waits until at most n vector memory operations
+// are outstanding and ignores the other counters.
+__device__ constexpr int vmcnt_only(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0F70; }
+
+// Record extents (16-byte units) of the R row blocks of unit (set, kt): lane r
+// (r < R) holds the start of row block r's record and lane R + r its end; a
+// row block past the matrix gets an empty extent. One vector load per unit,
+// issued a unit before use, so its latency never stalls the stream (a scalar
+// load here waited on the scalar cache for every record).
+__device__ inline uint32_t unit_offsets(const WaveArgs &a, __amdgpu_buffer_rsrc_t offr, int64_t set, int64_t kt,
+                                        int lane) {
+    const int64_t rb = set * kDmaRows + (lane & (kDmaRows - 1));
+    const bool real = lane < 2 * kDmaRows && rb < a.RB;
+    const int byte = real ? (int)((rb * a.KT + kt + (lane >= kDmaRows)) * 4) : 0x7FFFFFF0;  // out of range: 0
+    return __builtin_amdgcn_raw_buffer_load_b32(offr, byte, 0, 0);
+}
+
+// Loads the record at 16-byte units [o0, o1) into an LDS slot (L transfers of
+// 16 bytes per lane) and this lane's mask word into msk.
+template <int L>
+__device__ inline void dma_rec(const uint8_t *__restrict__ stream, uint32_t o0, uint32_t o1, int lane,
+                               uint8_t *slot, uint2 &msk) {
+    const __amdgpu_buffer_rsrc_t rec = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(stream + (uint64_t)o0 * 16), (short)0, (int)((o1 - o0) * 16), kBufferRsrcWord3);
+    msk = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rec, lane * 8, 0, 0));
+#pragma unroll
+    for (int i = 0; i < L; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rec, (__attribute__((address_space(3))) void *)(slot + 1024 * i), 16,
+                                                 kMaskBytes + 1024 * i + lane * 16, 0, 0, 0);
+}
+
+// Decodes the record in `slot` (mask msk) against the tile's B operands.
+__device__ inline void decode_record(lds_u32 *slot, const uint8_t *lut, uint2 msk, const v4u32 (&xb)[kSteps],
+                                     floatx4 &acc) {
+    const StepOffsets so = step_offsets(msk);
+    const uint32_t tlo0 = (msk.x << 3) & 0x78787878u, thi0 = (msk.x >> 1) & 0x78787878u;
+    const uint32_t tlo1 = (msk.y << 3) & 0x78787878u, thi1 = (msk.y >> 1) & 0x78787878u;
+    StepWords sw = read_step(slot, lut, so, tlo0, thi0, 0);
+#pragma unroll
+    for (int s = 0; s < kSteps; ++s) {
+        StepWords nx;
+        if (s + 1 < kSteps) nx = read_step(slot, lut, so, s + 1 < 4 ? tlo0 : tlo1, s + 1 < 4 ? thi0 : thi1, s + 1);
+        const half8 av = finish_step(sw);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, __builtin_bit_cast(half8, xb[s]), acc, 0, 0, 0);
+        if (s + 1 < kSteps) sw = nx;
+    }
+}
+
+template <int L>
+__global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint32_t *__restrict__ off,
+                                                         const uint8_t *__restrict__ stream) {
+    constexpr int R = kDmaRows;
+    constexpr int kSlot = 1024 * L + 16;  // values + the decode's 12-byte overread
+    __shared__ __attribute__((aligned(16))) uint8_t slot0[kSlot];
+    __shared__ __attribute__((aligned(16))) uint8_t slot1[kSlot];
+    __shared__ __attribute__((aligned(16))) uint8_t slot2[kSlot];
+    __shared__ __attribute__((aligned(16))) uint8_t slot3[kSlot];
+    __shared__ __attribute__((aligned(16))) uint8_t lut[16 * 8];
+    uint8_t *const slots[R] = {slot0, slot1, slot2, slot3};  // indexed by constants only
+    const int lane = threadIdx.x;
+    const int64_t w = blockIdx.x, G = gridDim.x;
+    const int64_t u0 = w * a.units / G, u1 = (w + 1) * a.units / G;
+    if (u0 >= u1) return;
+    if (lane < 16) reinterpret_cast<uint2 *>(lut)[lane] = nibble_selectors((uint32_t)lane);
+
+    const __amdgpu_buffer_rsrc_t xr =
+        __builtin_amdgcn_make_buffer_rsrc((void *)a.X, (short)0, (int)a.x_bytes, kBufferRsrcWord3);
+    const int n_lane = lane & 15, g4 = 4 * (lane >> 4);
+    const int xoff = n_lane < a.N ? (int)(n_lane * a.ldx * 2) + 16 * (lane >> 4) : (int)a.x_bytes;
+
+    floatx4 acc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) acc[r] = floatx4{0.f, 0.f, 0.f, 0.f};
+    int64_t set = u0 / a.KT, kt = u0 % a.KT;
+    int64_t pend_set = -1, pend_nseg = 0;  // partial stored, arrival not yet counted
+    uint2 msk[R];
+    const __amdgpu_buffer_rsrc_t offr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)off, (short)0, (int)((a.RB * a.KT + 1) * 4), kBufferRsrcWord3);
+    // The first unit's records 0..2 and X; record 3 is requested while record 0
+    // is decoded, and from then on the next unit's record r - 1 while record r is.
+    uint32_t oc = unit_offsets(a, offr, set, kt, lane);
+    uint32_t on;  // the next unit's extents (this unit's again at the range's end)
+    {
+        int64_t s1 = set, k1 = kt + 1;
+        if (k1 == a.KT) {
+            k1 = 0;
+            ++s1;
+        }
+        on = u0 + 1 < u1 ? unit_offsets(a, offr, s1, k1, lane) : oc;
+    }
+#pragma unroll
+    for (int r = 0; r < R - 1; ++r)
+        dma_rec<L>(stream, __builtin_amdgcn_readlane(oc, r), __builtin_amdgcn_readlane(oc, R + r), lane, slots[r],
+                   msk[r]);
+    v4u32 xb[kSteps];
+    fetch_x(a, xr, xoff, kt, lane, xb);
+    for (int64_t u = u0; u < u1; ++u) {
+        int64_t setn = set, ktn = kt + 1;
+        if (ktn == a.KT) {
+            ktn = 0;
+            ++setn;
+        }
+        const bool more = u + 1 < u1;
+        const int64_t sp = more ? setn : set, kp = more ? ktn : kt;  // past the end: reload this unit, unused
+        v4u32 xn[kSteps];
+        uint32_t old = 0;
+        // Extents of the unit after next: loaded a whole unit before use.
+        uint32_t onn;
+        {
+            int64_t s2 = setn, k2 = ktn + 1;
+            if (k2 == a.KT) {
+                k2 = 0;
+                ++s2;
+            }
+            const bool more2 = u + 2 < u1;
+            onn = unit_offsets(a, offr, more2 ? s2 : sp, more2 ? k2 : kp, lane);
+        }
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            // Arrival at the row set finished by the previous unit: its partial's
+            // stores were followed by record 3's L + 1 loads (and the offsets
+            // load, which this count conservatively waits for too); the counter's
+            // answer is read two records later, so waiting for it stalls nothing.
+            if (r == 1 && pend_set >= 0) {
+                __builtin_amdgcn_s_waitcnt(vmcnt_only(L + 1));
+                old = arrive_count(a, pend_set, lane);
+            }
+            if (r == 3 && pend_set >= 0) {
+                arrive_finish<R>(a, pend_set, pend_nseg, old, lane);
+                pend_set = -1;
+            }
+            if (r == 0)
+                dma_rec<L>(stream, __builtin_amdgcn_readlane(oc, R - 1), __builtin_amdgcn_readlane(oc, 2 * R - 1), lane,
+                           slots[R - 1], msk[R - 1]);
+            else
+                dma_rec<L>(stream, __builtin_amdgcn_readlane(on, r - 1), __builtin_amdgcn_readlane(on, R + r - 1), lane,
+                           slots[r - 1], msk[r - 1]);
+            if (r == 2) fetch_x(a, xr, xoff, kp, lane, xn);
+            decode_record(as_lds(slots[r]), lut, msk[r], xb, acc[r]);
+        }
+
+        if (!more || ktn == 0) {  // end of this wavefront's segment of the row set
+            const int64_t w_first = unit_owner(set * a.KT, a.units, G);
+            const int64_t w_last = unit_owner(set * a.KT + a.KT - 1, a.units, G);
+            if (w_first == w_last) {
+                if (n_lane < a.N) {
+#pragma unroll
+                    for (int r = 0; r < R; ++r) store_rows4(a, n_lane, (set * R + r) * kTileRows + g4, acc[r]);
+                }
+            } else {
+                const int64_t slot_floats = (int64_t)a.N * kTileRows * R;
+                float *part_slot = a.ws + (set * a.maxseg + (w - w_first)) * slot_floats;
+                const __amdgpu_buffer_rsrc_t part = __builtin_amdgcn_make_buffer_rsrc(
+                    part_slot, (short)0, (int)(slot_floats * 4), kBufferRsrcWord3);
+                if (n_lane < a.N) {
+#pragma unroll
+                    for (int r = 0; r < R; ++r)
+                        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, acc[r]), part,
+                                                               (n_lane * kTileRows * R + kTileRows * r + g4) * 4, 0,
+                                                               kCachePolicyDevice);
+                }
+                pend_set = set;
+                pend_nseg = w_last - w_first + 1;
+            }
+#pragma unroll
+            for (int r = 0; r < R; ++r) acc[r] = floatx4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int i = 0; i < kSteps; ++i) xb[i] = xn[i];
+        oc = on;
+        on = onn;
+        set = setn;
+        kt = ktn;
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // also drains the unused prefetches of the range's end
+    if (pend_set >= 0) arrive_row_set<R>(a, pend_set, pend_nseg, lane);
 }
 
 // One wavefront per tile: decode every lane-step and store it densely.
@@ -476,7 +915,7 @@ __global__ __launch_bounds__(64) void densify_kernel(const uint8_t *stream, cons
     const int64_t row = rb * kTileRows + (lane & 15);
     if (row >= M) return;
     for (int s = 0; s < kSteps; ++s) {
-        const half8 av = decode_step(lds_address(region), lut, so, s < 4 ? tlo0 : tlo1, s < 4 ? thi0 : thi1, s);
+        const half8 av = decode_step(as_lds(region), lut, so, s < 4 ? tlo0 : tlo1, s < 4 ? thi0 : thi1, s);
         const uint4 u = __builtin_bit_cast(uint4, av);
         const int64_t col = kt * kTileK + tile_col(lane >> 4, s, 0);
         uint16_t *dst = Wd + row * ldw + col;
@@ -534,23 +973,143 @@ static int pass_nt(int64_t N, int64_t n0) {
     return (int)((nb + 15) / 16);
 }
 
+// ---------------------------------------------------------------------------
+// Plans of the single-wavefront kernels (passes of at most 16 tokens).
+// ---------------------------------------------------------------------------
+
+enum WaveKind { kWaveRegs = 0, kWaveDma4 = 1, kWaveNone = 2 };
+
+// Row blocks per unit of the register-staged wave kernel, and the smallest
+// number of units a wavefront streams before a split costs it a partial.
+constexpr int kWaveRows = 1;
+constexpr int64_t kMinUnitsPerWave = 4;
+constexpr int kMinWaveLoads = 2;  // record load groups instantiated: 2..8
+constexpr int64_t kMinUnitsPerDmaWave = 2;
+
+// Record load groups (1 KB each) that cover every record of A.
+static int wave_loads(const usp_matrix *A) {
+    const int l = (int)ceil_div(A->max_chunks, kLanes);
+    return l < kMinWaveLoads ? kMinWaveLoads : l;
+}
+
+typedef void (*WaveKernelFn)(WaveArgs, const uint32_t *, const uint8_t *);
+
+static WaveKernelFn wave_kernel(WaveKind kind, int loads) {
+#define USP_BY_LOADS(KERNEL)      \
+    switch (loads) {              \
+        case 2: return KERNEL<2>; \
+        case 3: return KERNEL<3>; \
+        case 4: return KERNEL<4>; \
+        case 5: return KERNEL<5>; \
+        case 6: return KERNEL<6>; \
+        case 7: return KERNEL<7>; \
+        default: return KERNEL<8>; \
+    }
+    if (kind == kWaveDma4) {
+        USP_BY_LOADS(spmm_dma_kernel)
+    }
+#undef USP_BY_LOADS
+    switch (loads) {
+        case 2: return spmm_wave_kernel<kWaveRows, 2>;
+        case 3: return spmm_wave_kernel<kWaveRows, 3>;
+        case 4: return spmm_wave_kernel<kWaveRows, 4>;
+        case 5: return spmm_wave_kernel<kWaveRows, 5>;
+        case 6: return spmm_wave_kernel<kWaveRows, 6>;
+        case 7: return spmm_wave_kernel<kWaveRows, 7>;
+        default: return spmm_wave_kernel<kWaveRows, 8>;
+    }
+}
+
+// Wavefronts of a wave kernel resident per CU (queried once per variant).
+static int resident_waves(WaveKind kind, int loads) {
+    static int cached[2][9] = {{0}};
+    int &c = cached[kind][loads];
+    if (c == 0) {
+        int n = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, wave_kernel(kind, loads), kLanes, 0) != hipSuccess ||
+            n < 1)
+            n = 1;
+        c = n;
+    }
+    return c;
+}
+
+struct WavePlan {
+    WaveKind kind;
+    int loads, rows;  // record load groups; row blocks per unit
+    int64_t sets, units, grid, maxseg;
+    bool split;
+};
+
+// Which single-wavefront kernel suits A (measured on MI355X, 16 tokens):
+// the direct-to-LDS kernel once every wavefront gets at least 8 units of 4
+// row blocks (70B- and 66B-class FFN layers), the register-staged kernel for
+// small matrices (13B attention projections: more, shorter ranges); in
+// between the four-wavefront kernel that shares X through LDS is faster.
+constexpr int64_t kDmaUnitsPerSlot = 8;
+constexpr int64_t kRegsMaxTiles = 8192;
+static WaveKind wave_kind(const usp_matrix *A, int loads) {
+    const int64_t slots = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(kWaveDma4, loads);
+    if (ceil_div(A->RB, kDmaRows) * A->KT >= kDmaUnitsPerSlot * slots) return kWaveDma4;
+    if (A->RB * A->KT <= kRegsMaxTiles) return kWaveRegs;
+    return kWaveNone;
+}
+
+static WavePlan plan_wave(const usp_matrix *A) {
+    WavePlan p;
+    p.loads = wave_loads(A);
+    p.kind = wave_kind(A, p.loads);
+    if (p.kind == kWaveNone) p.kind = kWaveRegs;  // sizes the workspace for every kernel that may run
+    p.rows = p.kind == kWaveDma4 ? kDmaRows : kWaveRows;
+    const int64_t min_units = p.kind == kWaveDma4 ? kMinUnitsPerDmaWave : kMinUnitsPerWave;
+    p.sets = ceil_div(A->RB, p.rows);
+    p.units = p.sets * A->KT;
+    const int64_t slots = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(p.kind, p.loads);
+    const int64_t want = ceil_div(p.units, min_units);
+    p.grid = want < slots ? want : slots;
+    // A range of KT units meets at most ceil(KT / shortest range) + 1 wavefronts.
+    const int64_t shortest = p.units / p.grid;
+    p.maxseg = ceil_div(A->KT, shortest) + 1;
+    p.split = (p.units % p.grid != 0) || ((p.units / p.grid) % A->KT != 0);
+    return p;
+}
+
+// The wave kernels serve passes of at most 16 tokens with X 16-byte aligned,
+// ldx and K multiples of 8, and X's extent and the offset table addressable by
+// 32-bit offsets.
+static bool use_wave_kernel(const usp_matrix *A, const void *X, int64_t ldx, int64_t N) {
+    if (N > 16 || (reinterpret_cast<uintptr_t>(X) & 15) || ldx % 8 || A->K % 8) return false;
+    const int64_t x_bytes = ((N - 1) * ldx + A->K) * 2;
+    if (x_bytes + 2 * A->KT * kTileK >= ((int64_t)1 << 31) || (A->RB * A->KT + 1) * 4 >= ((int64_t)1 << 31))
+        return false;
+    return wave_kind(A, wave_loads(A)) != kWaveNone;
+}
+
 SpmmPlan plan_spmm(const usp_matrix *A, int64_t N) { return plan_pass(A, pass_nt(N, 0)); }
 
 // Workspace: one uint32 arrival counter per row group at offset 0 (shared by
 // every pass, zero between passes), padded to 256 bytes, then the fp32 partials
 // of the current pass [row group][slot][tokens][64 rows].
-static size_t counters_bytes(const usp_matrix *A) {
-    return ((size_t)ceil_div(A->RB, kWaves) * sizeof(uint32_t) + 255) / 256 * 256;
-}
+// Sized for one counter per row block, which also covers one per row group, so
+// every kernel of the library finds zeroed counters at the same place.
+static size_t counters_bytes(const usp_matrix *A) { return ((size_t)A->RB * sizeof(uint32_t) + 255) / 256 * 256; }
 
 static size_t partials_bytes(const SpmmPlan &p, int64_t nb) {
     return (size_t)p.row_groups * (size_t)p.maxseg * (size_t)nb * 64 * sizeof(float);
 }
 
+static size_t wave_partials_bytes(const usp_matrix *A, int64_t N) {
+    const WavePlan p = plan_wave(A);
+    if (!p.split) return 0;
+    return (size_t)p.sets * (size_t)p.maxseg * (size_t)N * kTileRows * p.rows * sizeof(float);
+}
+
 size_t spmm_workspace_bytes(const usp_matrix *A, int64_t N) {
-    // Passes run one after another and reuse the workspace: full passes of
-    // 16 * kMaxNT tokens, then one pass over the remainder.
-    size_t need = 0;
+    // Layout: counters, then the partials of whichever pass runs. Passes run one
+    // after another and reuse the workspace: full passes of 16 * kMaxNT tokens,
+    // then one pass over the remainder; up to 16 tokens may take the wave kernel
+    // (sized here too, whichever needs more).
+    size_t need = N <= 16 ? wave_partials_bytes(A, N) : 0;
     auto add = [&](int64_t nb) {
         const SpmmPlan p = plan_pass(A, (int)((nb + 15) / 16));
         if (p.split) need = std::max(need, partials_bytes(p, nb));
@@ -560,9 +1119,35 @@ size_t spmm_workspace_bytes(const usp_matrix *A, int64_t N) {
     return need ? counters_bytes(A) + need : 0;
 }
 
+static int launch_wave(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy, int64_t N,
+                       void *workspace, hipStream_t st) {
+    const WavePlan p = plan_wave(A);
+    WaveArgs a;
+    a.M = A->M;
+    a.K = A->K;
+    a.RB = A->RB;
+    a.KT = A->KT;
+    a.sets = p.sets;
+    a.units = p.units;
+    a.maxseg = p.maxseg;
+    a.X = reinterpret_cast<const uint16_t *>(X);
+    a.ldx = ldx;
+    a.x_bytes = (uint32_t)(((N - 1) * ldx + A->K) * 2);
+    a.Y = reinterpret_cast<uint16_t *>(Y);
+    a.ldy = ldy;
+    a.N = (int)N;
+    a.cnt = p.split ? reinterpret_cast<uint32_t *>(workspace) : nullptr;
+    a.ws = p.split ? reinterpret_cast<float *>(reinterpret_cast<uint8_t *>(workspace) + counters_bytes(A)) : nullptr;
+    a.y_vec = ((reinterpret_cast<uintptr_t>(Y) & 7) == 0) && (ldy % 4 == 0);
+    hipLaunchKernelGGL(wave_kernel(p.kind, p.loads), dim3((unsigned)p.grid), dim3(kLanes), 0, st, a, A->d_off,
+                       reinterpret_cast<const uint8_t *>(A->d_stream));
+    return (int)hipGetLastError();
+}
+
 int launch_spmm(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy, int64_t N,
                 void *workspace, void *stream) {
     hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    if (use_wave_kernel(A, X, ldx, N)) return launch_wave(A, X, ldx, Y, ldy, N, workspace, st);
     for (int64_t n0 = 0; n0 < N; n0 += 16 * kMaxNT) {
         const int nb = (int)((N - n0) < 16 * kMaxNT ? (N - n0) : 16 * kMaxNT);
         const int nt = (nb + 15) / 16;

@@ -199,3 +199,22 @@ def test_workload_sampled_rows(torch, usp, name, N, s):
     got = Y.cpu().numpy().astype(np.float64)[:, rows]
     A.free()
     assert_close(got, inst.W, inst.mask, inst.X, rows=rows)
+
+
+# Matrices large enough that the planner picks the direct-to-LDS kernel (every
+# wavefront gets at least 8 units of 4 row blocks), checked on every output:
+# M = 36880 leaves the last set of 4 row blocks one block short, K = 8088 ends
+# in a partial column tile. Small integers in {-1, 0, 1} keep every partial sum
+# exact in fp32 and the outputs exact in fp16, so that case is bit-exact.
+def test_dma_kernel_exact_full(torch, usp):
+    W, mask, X = wl.make_small_int(36880, 8088, 16, 0.5, seed=21, lo=-1, hi=1)
+    Y = run(torch, usp, W, mask, X)
+    Yref, _ = oracle.masked_gemm(W, mask, X)
+    assert np.array_equal(Y, Yref)
+
+
+@pytest.mark.parametrize("density,N", [(0.7, 11), (0.95, 8)])
+def test_dma_kernel_dense_records_full(torch, usp, density, N):
+    W, mask, X = wl.make_random(36880, 8088, N, density, seed=22)
+    Y = run(torch, usp, W, mask, X)
+    assert_close(Y, W, mask, X)
