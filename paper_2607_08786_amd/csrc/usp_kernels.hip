@@ -113,7 +113,8 @@ __device__ inline lds_u32 *as_lds(const void *p) {
 // (8 KB), so a read never leaves the region's neighbourhood.
 __device__ inline void read_nibble(lds_u32 *region, uint32_t hb, uint32_t idx8, const uint8_t *lut,
                                    uint32_t *e, uint2 &sel) {
-    lds_u32 *d = region + ((hb & (kWRegionBytes - 4)) >> 2);
+    typedef const __attribute__((address_space(3))) uint8_t lds_u8;
+    lds_u32 *d = (lds_u32 *)((lds_u8 *)region + (hb & (kWRegionBytes - 4)));
     e[0] = d[0];
     e[1] = d[1];
     e[2] = d[2];
@@ -528,23 +529,31 @@ __device__ inline void arrive_finish(const WaveArgs &a, int64_t set, int64_t nse
         __builtin_amdgcn_make_buffer_rsrc(slot0, (short)0, (int)(nseg * slot_floats * 4), kBufferRsrcWord3);
     const int n = lane & 15, g4 = 4 * (lane >> 4);
     if (n < a.N) {
-#pragma unroll 1
-        for (int r = 0; r < R; ++r) {  // not unrolled: keeps this rare path's registers few
-            const int lofs = (n * kTileRows * R + kTileRows * r + g4) * 4;
-            floatx4 sum = {0.f, 0.f, 0.f, 0.f};
-            for (int64_t j0 = 0; j0 < nseg; j0 += 8) {
-                v4u32 v[8];
+        // Batches of B slots x R row blocks (16 loads), issued together, then
+        // added in slot order per row block: one round trip for up to B slots.
+        constexpr int B = R >= 16 ? 1 : 16 / R;
+        floatx4 sum[R];
 #pragma unroll
-                for (int jj = 0; jj < 8; ++jj)  // a batch of loads, then adds in slot order
-                    v[jj] = j0 + jj < nseg ? __builtin_amdgcn_raw_buffer_load_b128(
-                                                 part, (int)((j0 + jj) * slot_floats * 4) + lofs, 0, kCachePolicyDevice)
-                                           : v4u32{0u, 0u, 0u, 0u};
+        for (int r = 0; r < R; ++r) sum[r] = floatx4{0.f, 0.f, 0.f, 0.f};
+        const int lofs = (n * kTileRows * R + g4) * 4;
+        for (int64_t j0 = 0; j0 < nseg; j0 += B) {
+            v4u32 v[B][R];
 #pragma unroll
-                for (int jj = 0; jj < 8; ++jj)
-                    if (j0 + jj < nseg) sum += __builtin_bit_cast(floatx4, v[jj]);
-            }
-            store_rows4(a, n, (set * R + r) * kTileRows + g4, sum);
+            for (int jj = 0; jj < B; ++jj)
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+                    v[jj][r] = j0 + jj < nseg ? __builtin_amdgcn_raw_buffer_load_b128(
+                                                    part, (int)((j0 + jj) * slot_floats * 4) + lofs + 64 * r, 0,
+                                                    kCachePolicyDevice)
+                                              : v4u32{0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int jj = 0; jj < B; ++jj)
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+                    if (j0 + jj < nseg) sum[r] += __builtin_bit_cast(floatx4, v[jj][r]);
         }
+#pragma unroll
+        for (int r = 0; r < R; ++r) store_rows4(a, n, (set * R + r) * kTileRows + g4, sum[r]);
     }
     if (lane == 0) __hip_atomic_store(a.cnt + set, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -725,9 +734,9 @@ __device__ constexpr int vmcnt_only(int n) { return (n & 15) | ((n >> 4) << 14) 
 // issued a unit before use, so its latency never stalls the stream (a scalar
 // load here waited on the scalar cache for every record).
 __device__ inline uint32_t unit_offsets(const WaveArgs &a, __amdgpu_buffer_rsrc_t offr, int64_t set, int64_t kt,
-                                        int lane) {
-    const int64_t rb = set * kDmaRows + (lane & (kDmaRows - 1));
-    const bool real = lane < 2 * kDmaRows && rb < a.RB;
+                                        int lane, bool valid = true) {
+    const int64_t rb = set * kDmaRows + lane % kDmaRows;
+    const bool real = valid && lane < 2 * kDmaRows && rb < a.RB;
     const int byte = real ? (int)((rb * a.KT + kt + (lane >= kDmaRows)) * 4) : 0x7FFFFFF0;  // out of range: 0
     return __builtin_amdgcn_raw_buffer_load_b32(offr, byte, 0, 0);
 }
@@ -773,7 +782,7 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
     __shared__ __attribute__((aligned(16))) uint8_t slot2[kSlot];
     __shared__ __attribute__((aligned(16))) uint8_t slot3[kSlot];
     __shared__ __attribute__((aligned(16))) uint8_t lut[16 * 8];
-    uint8_t *const slots[R] = {slot0, slot1, slot2, slot3};  // indexed by constants only
+    uint8_t *const slots[4] = {slot0, slot1, slot2, slot3};  // indexed by constants < R only
     const int lane = threadIdx.x;
     const int64_t w = blockIdx.x, G = gridDim.x;
     const int64_t u0 = w * a.units / G, u1 = (w + 1) * a.units / G;
@@ -803,7 +812,7 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
             k1 = 0;
             ++s1;
         }
-        on = u0 + 1 < u1 ? unit_offsets(a, offr, s1, k1, lane) : oc;
+        on = unit_offsets(a, offr, s1, k1, lane, u0 + 1 < u1);  // past the range: empty extents
     }
 #pragma unroll
     for (int r = 0; r < R - 1; ++r)
@@ -829,8 +838,7 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
                 k2 = 0;
                 ++s2;
             }
-            const bool more2 = u + 2 < u1;
-            onn = unit_offsets(a, offr, more2 ? s2 : sp, more2 ? k2 : kp, lane);
+            onn = unit_offsets(a, offr, s2, k2, lane, u + 2 < u1);  // past the range: empty extents
         }
 #pragma unroll
         for (int r = 0; r < R; ++r) {
@@ -842,7 +850,7 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
                 __builtin_amdgcn_s_waitcnt(vmcnt_only(L + 1));
                 old = arrive_count(a, pend_set, lane);
             }
-            if (r == 3 && pend_set >= 0) {
+            if (r == R - 1 && pend_set >= 0) {
                 arrive_finish<R>(a, pend_set, pend_nseg, old, lane);
                 pend_set = -1;
             }
