@@ -519,7 +519,7 @@ __device__ inline uint32_t arrive_count(const WaveArgs &a, int64_t set, int lane
 
 // With the counter's previous value: the last of the nseg arrivals sums every
 // slot in order, stores Y and resets the counter.
-template <int R>
+template <int R, int NB = 1>
 __device__ inline void arrive_finish(const WaveArgs &a, int64_t set, int64_t nseg, uint32_t old, int lane) {
     old = __builtin_amdgcn_readfirstlane(old);
     if (old != (uint32_t)nseg - 1u) return;
@@ -527,40 +527,44 @@ __device__ inline void arrive_finish(const WaveArgs &a, int64_t set, int64_t nse
     float *slot0 = a.ws + set * a.maxseg * slot_floats;
     const __amdgpu_buffer_rsrc_t part =
         __builtin_amdgcn_make_buffer_rsrc(slot0, (short)0, (int)(nseg * slot_floats * 4), kBufferRsrcWord3);
-    const int n = lane & 15, g4 = 4 * (lane >> 4);
-    if (n < a.N) {
-        // Batches of B slots x R row blocks (16 loads), issued together, then
-        // added in slot order per row block: one round trip for up to B slots.
-        constexpr int B = R >= 16 ? 1 : 16 / R;
-        floatx4 sum[R];
+    const int g4 = 4 * (lane >> 4);
+#pragma unroll 1
+    for (int nb = 0; nb < NB; ++nb) {
+        const int n = 16 * nb + (lane & 15);
+        if (n < a.N) {
+            // Batches of B slots x R row blocks (16 loads), issued together, then
+            // added in slot order per row block: one round trip for up to B slots.
+            constexpr int B = R >= 16 ? 1 : 16 / R;
+            floatx4 sum[R];
 #pragma unroll
-        for (int r = 0; r < R; ++r) sum[r] = floatx4{0.f, 0.f, 0.f, 0.f};
-        const int lofs = (n * kTileRows * R + g4) * 4;
-        for (int64_t j0 = 0; j0 < nseg; j0 += B) {
-            v4u32 v[B][R];
+            for (int r = 0; r < R; ++r) sum[r] = floatx4{0.f, 0.f, 0.f, 0.f};
+            const int lofs = (n * kTileRows * R + g4) * 4;
+            for (int64_t j0 = 0; j0 < nseg; j0 += B) {
+                v4u32 v[B][R];
 #pragma unroll
-            for (int jj = 0; jj < B; ++jj)
+                for (int jj = 0; jj < B; ++jj)
 #pragma unroll
-                for (int r = 0; r < R; ++r)
-                    v[jj][r] = j0 + jj < nseg ? __builtin_amdgcn_raw_buffer_load_b128(
-                                                    part, (int)((j0 + jj) * slot_floats * 4) + lofs + 64 * r, 0,
-                                                    kCachePolicyDevice)
-                                              : v4u32{0u, 0u, 0u, 0u};
+                    for (int r = 0; r < R; ++r)
+                        v[jj][r] = j0 + jj < nseg ? __builtin_amdgcn_raw_buffer_load_b128(
+                                                        part, (int)((j0 + jj) * slot_floats * 4) + lofs + 64 * r, 0,
+                                                        kCachePolicyDevice)
+                                                  : v4u32{0u, 0u, 0u, 0u};
 #pragma unroll
-            for (int jj = 0; jj < B; ++jj)
+                for (int jj = 0; jj < B; ++jj)
 #pragma unroll
-                for (int r = 0; r < R; ++r)
-                    if (j0 + jj < nseg) sum[r] += __builtin_bit_cast(floatx4, v[jj][r]);
+                    for (int r = 0; r < R; ++r)
+                        if (j0 + jj < nseg) sum[r] += __builtin_bit_cast(floatx4, v[jj][r]);
+            }
+#pragma unroll
+            for (int r = 0; r < R; ++r) store_rows4(a, n, (set * R + r) * kTileRows + g4, sum[r]);
         }
-#pragma unroll
-        for (int r = 0; r < R; ++r) store_rows4(a, n, (set * R + r) * kTileRows + g4, sum[r]);
     }
     if (lane == 0) __hip_atomic_store(a.cnt + set, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-template <int R>
+template <int R, int NB = 1>
 __device__ inline void arrive_row_set(const WaveArgs &a, int64_t set, int64_t nseg, int lane) {
-    arrive_finish<R>(a, set, nseg, arrive_count(a, set, lane), lane);
+    arrive_finish<R, NB>(a, set, nseg, arrive_count(a, set, lane), lane);
 }
 
 // One tile record in registers: this lane's mask word and L KB of the packed
@@ -756,8 +760,9 @@ __device__ inline void dma_rec(const uint8_t *__restrict__ stream, uint32_t o0, 
 }
 
 // Decodes the record in `slot` (mask msk) against the tile's B operands.
-__device__ inline void decode_record(lds_u32 *slot, const uint8_t *lut, uint2 msk, const v4u32 (&xb)[kSteps],
-                                     floatx4 &acc) {
+template <int NB>
+__device__ inline void decode_record(lds_u32 *slot, const uint8_t *lut, uint2 msk, const v4u32 (&xb)[NB][kSteps],
+                                     floatx4 (&acc)[NB]) {
     const StepOffsets so = step_offsets(msk);
     const uint32_t tlo0 = (msk.x << 3) & 0x78787878u, thi0 = (msk.x >> 1) & 0x78787878u;
     const uint32_t tlo1 = (msk.y << 3) & 0x78787878u, thi1 = (msk.y >> 1) & 0x78787878u;
@@ -767,12 +772,15 @@ __device__ inline void decode_record(lds_u32 *slot, const uint8_t *lut, uint2 ms
         StepWords nx;
         if (s + 1 < kSteps) nx = read_step(slot, lut, so, s + 1 < 4 ? tlo0 : tlo1, s + 1 < 4 ? thi0 : thi1, s + 1);
         const half8 av = finish_step(sw);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, __builtin_bit_cast(half8, xb[s]), acc, 0, 0, 0);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, __builtin_bit_cast(half8, xb[nb][s]), acc[nb], 0, 0, 0);
         if (s + 1 < kSteps) sw = nx;
     }
 }
 
-template <int L>
+// NB blocks of 16 tokens: each decoded step feeds NB MFMAs.
+template <int L, int NB>
 __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint32_t *__restrict__ off,
                                                          const uint8_t *__restrict__ stream) {
     constexpr int R = kDmaRows;
@@ -792,34 +800,43 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
     const __amdgpu_buffer_rsrc_t xr =
         __builtin_amdgcn_make_buffer_rsrc((void *)a.X, (short)0, (int)a.x_bytes, kBufferRsrcWord3);
     const int n_lane = lane & 15, g4 = 4 * (lane >> 4);
-    const int xoff = n_lane < a.N ? (int)(n_lane * a.ldx * 2) + 16 * (lane >> 4) : (int)a.x_bytes;
-
-    floatx4 acc[R];
+    // Lanes of tokens >= N start at the resource's end: their loads return zeros.
+    int xoff[NB];
 #pragma unroll
-    for (int r = 0; r < R; ++r) acc[r] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int nb = 0; nb < NB; ++nb) {
+        const int tok = 16 * nb + n_lane;
+        xoff[nb] = tok < a.N ? (int)(tok * a.ldx * 2) + 16 * (lane >> 4) : (int)a.x_bytes;
+    }
+
+    floatx4 acc[R][NB];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[r][nb] = floatx4{0.f, 0.f, 0.f, 0.f};
     int64_t set = u0 / a.KT, kt = u0 % a.KT;
     int64_t pend_set = -1, pend_nseg = 0;  // partial stored, arrival not yet counted
     uint2 msk[R];
     const __amdgpu_buffer_rsrc_t offr = __builtin_amdgcn_make_buffer_rsrc(
         (void *)off, (short)0, (int)((a.RB * a.KT + 1) * 4), kBufferRsrcWord3);
-    // The first unit's records 0..2 and X; record 3 is requested while record 0
+    // The first unit's records 0..R-2 and X; record R-1 is requested while record 0
     // is decoded, and from then on the next unit's record r - 1 while record r is.
     uint32_t oc = unit_offsets(a, offr, set, kt, lane);
-    uint32_t on;  // the next unit's extents (this unit's again at the range's end)
+    uint32_t on;  // the next unit's extents (empty past the range's end)
     {
         int64_t s1 = set, k1 = kt + 1;
         if (k1 == a.KT) {
             k1 = 0;
             ++s1;
         }
-        on = unit_offsets(a, offr, s1, k1, lane, u0 + 1 < u1);  // past the range: empty extents
+        on = unit_offsets(a, offr, s1, k1, lane, u0 + 1 < u1);
     }
 #pragma unroll
     for (int r = 0; r < R - 1; ++r)
         dma_rec<L>(stream, __builtin_amdgcn_readlane(oc, r), __builtin_amdgcn_readlane(oc, R + r), lane, slots[r],
                    msk[r]);
-    v4u32 xb[kSteps];
-    fetch_x(a, xr, xoff, kt, lane, xb);
+    v4u32 xb[NB][kSteps];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) fetch_x(a, xr, xoff[nb], kt, lane, xb[nb]);
     for (int64_t u = u0; u < u1; ++u) {
         int64_t setn = set, ktn = kt + 1;
         if (ktn == a.KT) {
@@ -827,8 +844,12 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
             ++setn;
         }
         const bool more = u + 1 < u1;
-        const int64_t sp = more ? setn : set, kp = more ? ktn : kt;  // past the end: reload this unit, unused
-        v4u32 xn[kSteps];
+        const int64_t kp = more ? ktn : kt;  // X of the next unit (past the range's end: this one's, unused)
+        // One token block: the next unit's X is loaded into a second buffer while
+        // this unit is decoded. More: a second buffer would not fit the
+        // registers, so the one buffer is reloaded after the unit's last decode.
+        constexpr bool kXAhead = NB == 1;
+        v4u32 xn[kXAhead ? NB : 1][kSteps];
         uint32_t old = 0;
         // Extents of the unit after next: loaded a whole unit before use.
         uint32_t onn;
@@ -843,15 +864,15 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             // Arrival at the row set finished by the previous unit: its partial's
-            // stores were followed by record 3's L + 1 loads (and the offsets
+            // stores were followed by record R-1's L + 1 loads (and the offsets
             // load, which this count conservatively waits for too); the counter's
-            // answer is read two records later, so waiting for it stalls nothing.
+            // answer is read a record or two later, so waiting for it stalls nothing.
             if (r == 1 && pend_set >= 0) {
                 __builtin_amdgcn_s_waitcnt(vmcnt_only(L + 1));
                 old = arrive_count(a, pend_set, lane);
             }
             if (r == R - 1 && pend_set >= 0) {
-                arrive_finish<R>(a, pend_set, pend_nseg, old, lane);
+                arrive_finish<R, NB>(a, pend_set, pend_nseg, old, lane);
                 pend_set = -1;
             }
             if (r == 0)
@@ -860,45 +881,66 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
             else
                 dma_rec<L>(stream, __builtin_amdgcn_readlane(on, r - 1), __builtin_amdgcn_readlane(on, R + r - 1), lane,
                            slots[r - 1], msk[r - 1]);
-            if (r == 2) fetch_x(a, xr, xoff, kp, lane, xn);
-            decode_record(as_lds(slots[r]), lut, msk[r], xb, acc[r]);
+            if (kXAhead && r == 2) {
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb) fetch_x(a, xr, xoff[nb], kp, lane, xn[kXAhead ? nb : 0]);
+            }
+            decode_record<NB>(as_lds(slots[r]), lut, msk[r], xb, acc[r]);
+        }
+        if (!kXAhead) {
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) fetch_x(a, xr, xoff[nb], kp, lane, xb[nb]);
         }
 
         if (!more || ktn == 0) {  // end of this wavefront's segment of the row set
             const int64_t w_first = unit_owner(set * a.KT, a.units, G);
             const int64_t w_last = unit_owner(set * a.KT + a.KT - 1, a.units, G);
             if (w_first == w_last) {
-                if (n_lane < a.N) {
 #pragma unroll
-                    for (int r = 0; r < R; ++r) store_rows4(a, n_lane, (set * R + r) * kTileRows + g4, acc[r]);
+                for (int nb = 0; nb < NB; ++nb) {
+                    const int tok = 16 * nb + n_lane;
+                    if (tok < a.N) {
+#pragma unroll
+                        for (int r = 0; r < R; ++r) store_rows4(a, tok, (set * R + r) * kTileRows + g4, acc[r][nb]);
+                    }
                 }
             } else {
                 const int64_t slot_floats = (int64_t)a.N * kTileRows * R;
                 float *part_slot = a.ws + (set * a.maxseg + (w - w_first)) * slot_floats;
                 const __amdgpu_buffer_rsrc_t part = __builtin_amdgcn_make_buffer_rsrc(
                     part_slot, (short)0, (int)(slot_floats * 4), kBufferRsrcWord3);
-                if (n_lane < a.N) {
 #pragma unroll
-                    for (int r = 0; r < R; ++r)
-                        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, acc[r]), part,
-                                                               (n_lane * kTileRows * R + kTileRows * r + g4) * 4, 0,
-                                                               kCachePolicyDevice);
+                for (int nb = 0; nb < NB; ++nb) {
+                    const int tok = 16 * nb + n_lane;
+                    if (tok < a.N) {
+#pragma unroll
+                        for (int r = 0; r < R; ++r)
+                            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, acc[r][nb]), part,
+                                                                   (tok * kTileRows * R + kTileRows * r + g4) * 4, 0,
+                                                                   kCachePolicyDevice);
+                    }
                 }
                 pend_set = set;
                 pend_nseg = w_last - w_first + 1;
             }
 #pragma unroll
-            for (int r = 0; r < R; ++r) acc[r] = floatx4{0.f, 0.f, 0.f, 0.f};
-        }
+            for (int r = 0; r < R; ++r)
 #pragma unroll
-        for (int i = 0; i < kSteps; ++i) xb[i] = xn[i];
+                for (int nb = 0; nb < NB; ++nb) acc[r][nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        }
+        if (kXAhead) {
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int i = 0; i < kSteps; ++i) xb[nb][i] = xn[kXAhead ? nb : 0][i];
+        }
         oc = on;
         on = onn;
         set = setn;
         kt = ktn;
     }
     __builtin_amdgcn_s_waitcnt(0);  // also drains the unused prefetches of the range's end
-    if (pend_set >= 0) arrive_row_set<R>(a, pend_set, pend_nseg, lane);
+    if (pend_set >= 0) arrive_row_set<R, NB>(a, pend_set, pend_nseg, lane);
 }
 
 // One wavefront per tile: decode every lane-step and store it densely.
@@ -1002,19 +1044,26 @@ static int wave_loads(const usp_matrix *A) {
 
 typedef void (*WaveKernelFn)(WaveArgs, const uint32_t *, const uint8_t *);
 
-static WaveKernelFn wave_kernel(WaveKind kind, int loads) {
-#define USP_BY_LOADS(KERNEL)      \
-    switch (loads) {              \
-        case 2: return KERNEL<2>; \
-        case 3: return KERNEL<3>; \
-        case 4: return KERNEL<4>; \
-        case 5: return KERNEL<5>; \
-        case 6: return KERNEL<6>; \
-        case 7: return KERNEL<7>; \
-        default: return KERNEL<8>; \
+// Token blocks of 16 the direct-to-LDS kernel is built for (X for all of them
+// stays in registers): 1 or 2.
+constexpr int kMaxDmaTokenBlocks = 2;
+
+static WaveKernelFn wave_kernel(WaveKind kind, int loads, int nb) {
+#define USP_BY_LOADS(KERNEL, ...)              \
+    switch (loads) {                           \
+        case 2: return KERNEL<2, ##__VA_ARGS__>; \
+        case 3: return KERNEL<3, ##__VA_ARGS__>; \
+        case 4: return KERNEL<4, ##__VA_ARGS__>; \
+        case 5: return KERNEL<5, ##__VA_ARGS__>; \
+        case 6: return KERNEL<6, ##__VA_ARGS__>; \
+        case 7: return KERNEL<7, ##__VA_ARGS__>; \
+        default: return KERNEL<8, ##__VA_ARGS__>; \
     }
     if (kind == kWaveDma4) {
-        USP_BY_LOADS(spmm_dma_kernel)
+        if (nb == 1) {
+            USP_BY_LOADS(spmm_dma_kernel, 1)
+        }
+        USP_BY_LOADS(spmm_dma_kernel, 2)
     }
 #undef USP_BY_LOADS
     switch (loads) {
@@ -1029,12 +1078,12 @@ static WaveKernelFn wave_kernel(WaveKind kind, int loads) {
 }
 
 // Wavefronts of a wave kernel resident per CU (queried once per variant).
-static int resident_waves(WaveKind kind, int loads) {
-    static int cached[2][9] = {{0}};
-    int &c = cached[kind][loads];
+static int resident_waves(WaveKind kind, int loads, int nb) {
+    static int cached[2][9][kMaxDmaTokenBlocks + 1] = {};
+    int &c = cached[kind][loads][nb];
     if (c == 0) {
         int n = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, wave_kernel(kind, loads), kLanes, 0) != hipSuccess ||
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, wave_kernel(kind, loads, nb), kLanes, 0) != hipSuccess ||
             n < 1)
             n = 1;
         c = n;
@@ -1044,35 +1093,40 @@ static int resident_waves(WaveKind kind, int loads) {
 
 struct WavePlan {
     WaveKind kind;
-    int loads, rows;  // record load groups; row blocks per unit
+    int loads, rows, nb;  // record load groups; row blocks per unit; token blocks
     int64_t sets, units, grid, maxseg;
     bool split;
 };
 
-// Which single-wavefront kernel suits A (measured on MI355X, 16 tokens):
+// Which single-wavefront kernel suits A for N tokens (measured on MI355X):
 // the direct-to-LDS kernel once every wavefront gets at least 8 units of 4
-// row blocks (70B- and 66B-class FFN layers), the register-staged kernel for
-// small matrices (13B attention projections: more, shorter ranges); in
-// between the four-wavefront kernel that shares X through LDS is faster.
+// row blocks (70B- and 66B-class FFN layers, up to 32 tokens), the
+// register-staged kernel for small matrices and up to 16 tokens (13B attention
+// projections: more, shorter ranges); otherwise the four-wavefront kernel,
+// which shares X through LDS.
 constexpr int64_t kDmaUnitsPerSlot = 8;
 constexpr int64_t kRegsMaxTiles = 8192;
-static WaveKind wave_kind(const usp_matrix *A, int loads) {
-    const int64_t slots = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(kWaveDma4, loads);
-    if (ceil_div(A->RB, kDmaRows) * A->KT >= kDmaUnitsPerSlot * slots) return kWaveDma4;
-    if (A->RB * A->KT <= kRegsMaxTiles) return kWaveRegs;
+static WaveKind wave_kind(const usp_matrix *A, int loads, int64_t N) {
+    const int nb = (int)ceil_div(N, 16);
+    if (nb <= kMaxDmaTokenBlocks) {
+        const int64_t slots = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(kWaveDma4, loads, nb);
+        if (ceil_div(A->RB, kDmaRows) * A->KT >= kDmaUnitsPerSlot * slots) return kWaveDma4;
+    }
+    if (nb == 1 && A->RB * A->KT <= kRegsMaxTiles) return kWaveRegs;
     return kWaveNone;
 }
 
-static WavePlan plan_wave(const usp_matrix *A) {
+static WavePlan plan_wave(const usp_matrix *A, int64_t N) {
     WavePlan p;
     p.loads = wave_loads(A);
-    p.kind = wave_kind(A, p.loads);
+    p.kind = wave_kind(A, p.loads, N);
     if (p.kind == kWaveNone) p.kind = kWaveRegs;  // sizes the workspace for every kernel that may run
+    p.nb = p.kind == kWaveDma4 ? (int)ceil_div(N, 16) : 1;
     p.rows = p.kind == kWaveDma4 ? kDmaRows : kWaveRows;
     const int64_t min_units = p.kind == kWaveDma4 ? kMinUnitsPerDmaWave : kMinUnitsPerWave;
     p.sets = ceil_div(A->RB, p.rows);
     p.units = p.sets * A->KT;
-    const int64_t slots = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(p.kind, p.loads);
+    const int64_t slots = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(p.kind, p.loads, p.nb);
     const int64_t want = ceil_div(p.units, min_units);
     p.grid = want < slots ? want : slots;
     // A range of KT units meets at most ceil(KT / shortest range) + 1 wavefronts.
@@ -1082,15 +1136,15 @@ static WavePlan plan_wave(const usp_matrix *A) {
     return p;
 }
 
-// The wave kernels serve passes of at most 16 tokens with X 16-byte aligned,
-// ldx and K multiples of 8, and X's extent and the offset table addressable by
-// 32-bit offsets.
+// The wave kernels serve single passes (up to 32 tokens) with X 16-byte
+// aligned, ldx and K multiples of 8, and X's extent and the offset table
+// addressable by 32-bit offsets.
 static bool use_wave_kernel(const usp_matrix *A, const void *X, int64_t ldx, int64_t N) {
-    if (N > 16 || (reinterpret_cast<uintptr_t>(X) & 15) || ldx % 8 || A->K % 8) return false;
+    if (N > 16 * kMaxDmaTokenBlocks || (reinterpret_cast<uintptr_t>(X) & 15) || ldx % 8 || A->K % 8) return false;
     const int64_t x_bytes = ((N - 1) * ldx + A->K) * 2;
     if (x_bytes + 2 * A->KT * kTileK >= ((int64_t)1 << 31) || (A->RB * A->KT + 1) * 4 >= ((int64_t)1 << 31))
         return false;
-    return wave_kind(A, wave_loads(A)) != kWaveNone;
+    return wave_kind(A, wave_loads(A), N) != kWaveNone;
 }
 
 SpmmPlan plan_spmm(const usp_matrix *A, int64_t N) { return plan_pass(A, pass_nt(N, 0)); }
@@ -1107,7 +1161,7 @@ static size_t partials_bytes(const SpmmPlan &p, int64_t nb) {
 }
 
 static size_t wave_partials_bytes(const usp_matrix *A, int64_t N) {
-    const WavePlan p = plan_wave(A);
+    const WavePlan p = plan_wave(A, N);
     if (!p.split) return 0;
     return (size_t)p.sets * (size_t)p.maxseg * (size_t)N * kTileRows * p.rows * sizeof(float);
 }
@@ -1117,7 +1171,7 @@ size_t spmm_workspace_bytes(const usp_matrix *A, int64_t N) {
     // after another and reuse the workspace: full passes of 16 * kMaxNT tokens,
     // then one pass over the remainder; up to 16 tokens may take the wave kernel
     // (sized here too, whichever needs more).
-    size_t need = N <= 16 ? wave_partials_bytes(A, N) : 0;
+    size_t need = N <= 16 * kMaxDmaTokenBlocks ? wave_partials_bytes(A, N) : 0;
     auto add = [&](int64_t nb) {
         const SpmmPlan p = plan_pass(A, (int)((nb + 15) / 16));
         if (p.split) need = std::max(need, partials_bytes(p, nb));
@@ -1129,7 +1183,7 @@ size_t spmm_workspace_bytes(const usp_matrix *A, int64_t N) {
 
 static int launch_wave(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy, int64_t N,
                        void *workspace, hipStream_t st) {
-    const WavePlan p = plan_wave(A);
+    const WavePlan p = plan_wave(A, N);
     WaveArgs a;
     a.M = A->M;
     a.K = A->K;
@@ -1147,7 +1201,7 @@ static int launch_wave(const usp_matrix *A, const void *X, int64_t ldx, void *Y,
     a.cnt = p.split ? reinterpret_cast<uint32_t *>(workspace) : nullptr;
     a.ws = p.split ? reinterpret_cast<float *>(reinterpret_cast<uint8_t *>(workspace) + counters_bytes(A)) : nullptr;
     a.y_vec = ((reinterpret_cast<uintptr_t>(Y) & 7) == 0) && (ldy % 4 == 0);
-    hipLaunchKernelGGL(wave_kernel(p.kind, p.loads), dim3((unsigned)p.grid), dim3(kLanes), 0, st, a, A->d_off,
+    hipLaunchKernelGGL(wave_kernel(p.kind, p.loads, p.nb), dim3((unsigned)p.grid), dim3(kLanes), 0, st, a, A->d_off,
                        reinterpret_cast<const uint8_t *>(A->d_stream));
     return (int)hipGetLastError();
 }

@@ -218,3 +218,18 @@ def test_dma_kernel_dense_records_full(torch, usp, density, N):
     W, mask, X = wl.make_random(36880, 8088, N, density, seed=22)
     Y = run(torch, usp, W, mask, X)
     assert_close(Y, W, mask, X)
+
+
+# Two blocks of 16 tokens through the direct-to-LDS kernel (each decoded step
+# feeds two MFMAs): exact on small integers at 32 tokens, tolerance at 27.
+def test_dma_kernel_two_token_blocks_exact(torch, usp):
+    W, mask, X = wl.make_small_int(36880, 8088, 32, 0.5, seed=23, lo=-1, hi=1)
+    Y = run(torch, usp, W, mask, X)
+    Yref, _ = oracle.masked_gemm(W, mask, X)
+    assert np.array_equal(Y, Yref)
+
+
+def test_dma_kernel_two_token_blocks_ragged(torch, usp):
+    W, mask, X = wl.make_random(36880, 8088, 27, 0.5, seed=24)
+    Y = run(torch, usp, W, mask, X)
+    assert_close(Y, W, mask, X)
