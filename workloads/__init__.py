@@ -8,9 +8,11 @@ GPU tests take their inputs from here.
 from .gen import (  # noqa: F401
     CONFIGS,
     Instance,
+    draw_weights,
     instance_list,
     keep_count,
     make_instance,
+    make_mask,
     make_random,
     make_small_int,
     make_x,
