@@ -595,6 +595,18 @@ __device__ inline void fetch_rec(const WaveArgs &a, const uint32_t *__restrict__
         r.w[i] = __builtin_amdgcn_raw_buffer_load_b128(rec, kMaskBytes + 1024 * i + lane * 16, 0, 0);
 }
 
+// Loads the record at 16-byte units [o0, o1) into registers.
+template <int L>
+__device__ inline void fetch_rec(const uint8_t *__restrict__ stream, uint32_t o0, uint32_t o1, int lane,
+                                 WaveRec<L> &r) {
+    const __amdgpu_buffer_rsrc_t rec = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(stream + (uint64_t)o0 * 16), (short)0, (int)((o1 - o0) * 16), kBufferRsrcWord3);
+    r.msk = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rec, lane * 8, 0, 0));
+#pragma unroll
+    for (int i = 0; i < L; ++i)
+        r.w[i] = __builtin_amdgcn_raw_buffer_load_b128(rec, kMaskBytes + 1024 * i + lane * 16, 0, 0);
+}
+
 // B operands of one tile: step s, lane (g = lane / 16, n = lane % 16) holds
 // X[n][256 kt + 32 s + 8 g .. + 7]; zero for n >= N (out of the X resource) and
 // for columns >= K.
@@ -607,6 +619,43 @@ __device__ inline void fetch_x(const WaveArgs &a, __amdgpu_buffer_rsrc_t xr, int
 #pragma unroll
         for (int s = 0; s < kSteps; ++s)
             if (kt * kTileK + 32 * s + 8 * (lane >> 4) >= a.K) xb[s] = v4u32{0u, 0u, 0u, 0u};
+    }
+}
+
+// Issue the LDS reads of all 8 steps of a record before expanding any (more
+// registers, shorter chain) instead of one step ahead.
+constexpr bool kDecodeAhead = false;
+
+// Decodes the record in `slot` (mask msk) against the tile's B operands.
+template <int NB>
+__device__ inline void decode_record(lds_u32 *slot, const uint8_t *lut, uint2 msk, const v4u32 (&xb)[NB][kSteps],
+                                     floatx4 (&acc)[NB]) {
+    const StepOffsets so = step_offsets(msk);
+    const uint32_t tlo0 = (msk.x << 3) & 0x78787878u, thi0 = (msk.x >> 1) & 0x78787878u;
+    const uint32_t tlo1 = (msk.y << 3) & 0x78787878u, thi1 = (msk.y >> 1) & 0x78787878u;
+    if (kDecodeAhead) {  // every step's LDS reads first: a short dependency chain per record
+        StepWords all[kSteps];
+#pragma unroll
+        for (int s = 0; s < kSteps; ++s) all[s] = read_step(slot, lut, so, s < 4 ? tlo0 : tlo1, s < 4 ? thi0 : thi1, s);
+#pragma unroll
+        for (int s = 0; s < kSteps; ++s) {
+            const half8 av = finish_step(all[s]);
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+                acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, __builtin_bit_cast(half8, xb[nb][s]), acc[nb], 0, 0, 0);
+        }
+        return;
+    }
+    StepWords sw = read_step(slot, lut, so, tlo0, thi0, 0);
+#pragma unroll
+    for (int s = 0; s < kSteps; ++s) {
+        StepWords nx;
+        if (s + 1 < kSteps) nx = read_step(slot, lut, so, s + 1 < 4 ? tlo0 : tlo1, s + 1 < 4 ? thi0 : thi1, s + 1);
+        const half8 av = finish_step(sw);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, __builtin_bit_cast(half8, xb[nb][s]), acc[nb], 0, 0, 0);
+        if (s + 1 < kSteps) sw = nx;
     }
 }
 
@@ -666,19 +715,8 @@ __global__ __launch_bounds__(kLanes) void spmm_wave_kernel(WaveArgs a, const uin
             if (r + 1 < R) fetch_rec<L>(a, off, stream, set * R + r + 1, kt, lane, cur);
             else fetch_rec<L>(a, off, stream, (more ? setn : set) * R, more ? ktn : kt, lane, cur);
 
-            const StepOffsets so = step_offsets(msk);
-            const uint32_t tlo0 = (msk.x << 3) & 0x78787878u, thi0 = (msk.x >> 1) & 0x78787878u;
-            const uint32_t tlo1 = (msk.y << 3) & 0x78787878u, thi1 = (msk.y >> 1) & 0x78787878u;
-            StepWords sw = read_step(rbase, lut, so, tlo0, thi0, 0);
-#pragma unroll
-            for (int s = 0; s < kSteps; ++s) {
-                StepWords nx;
-                if (s + 1 < kSteps)
-                    nx = read_step(rbase, lut, so, s + 1 < 4 ? tlo0 : tlo1, s + 1 < 4 ? thi0 : thi1, s + 1);
-                const half8 av = finish_step(sw);
-                acc[r] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, __builtin_bit_cast(half8, xb[s]), acc[r], 0, 0, 0);
-                if (s + 1 < kSteps) sw = nx;
-            }
+            decode_record<1>(rbase, lut, msk, reinterpret_cast<const v4u32(&)[1][kSteps]>(xb),
+                             reinterpret_cast<floatx4(&)[1]>(acc[r]));
         }
 
         if (!more || ktn == 0) {  // end of this wavefront's segment of the row set
@@ -759,25 +797,6 @@ __device__ inline void dma_rec(const uint8_t *__restrict__ stream, uint32_t o0, 
                                                  kMaskBytes + 1024 * i + lane * 16, 0, 0, 0);
 }
 
-// Decodes the record in `slot` (mask msk) against the tile's B operands.
-template <int NB>
-__device__ inline void decode_record(lds_u32 *slot, const uint8_t *lut, uint2 msk, const v4u32 (&xb)[NB][kSteps],
-                                     floatx4 (&acc)[NB]) {
-    const StepOffsets so = step_offsets(msk);
-    const uint32_t tlo0 = (msk.x << 3) & 0x78787878u, thi0 = (msk.x >> 1) & 0x78787878u;
-    const uint32_t tlo1 = (msk.y << 3) & 0x78787878u, thi1 = (msk.y >> 1) & 0x78787878u;
-    StepWords sw = read_step(slot, lut, so, tlo0, thi0, 0);
-#pragma unroll
-    for (int s = 0; s < kSteps; ++s) {
-        StepWords nx;
-        if (s + 1 < kSteps) nx = read_step(slot, lut, so, s + 1 < 4 ? tlo0 : tlo1, s + 1 < 4 ? thi0 : thi1, s + 1);
-        const half8 av = finish_step(sw);
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, __builtin_bit_cast(half8, xb[nb][s]), acc[nb], 0, 0, 0);
-        if (s + 1 < kSteps) sw = nx;
-    }
-}
 
 // NB blocks of 16 tokens: each decoded step feeds NB MFMAs.
 template <int L, int NB>
@@ -943,6 +962,94 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
     if (pend_set >= 0) arrive_row_set<R, NB>(a, pend_set, pend_nseg, lane);
 }
 
+// ---------------------------------------------------------------------------
+// Row-block kernel for small matrices (up to 16 tokens).
+//
+// One workgroup per row block: its W wavefronts split the row block's column
+// tiles and sum their partials through LDS behind one barrier, in a fixed order.
+// Small matrices cannot keep every CU busy without splitting K, and a split
+// across workgroups costs device-coherent partial stores, an atomic arrival and
+// a reduction at the very end of the kernel, where nothing hides it; inside a
+// workgroup the split is almost free. Each wavefront keeps its next two
+// records in flight in a register ring (one is staged in LDS and decoded) and
+// loads the next record's X operands one record ahead. The first record's
+// extent comes through the scalar cache; the others from one vector load of the
+// wavefront's stretch of the offset table, issued at the start.
+// ---------------------------------------------------------------------------
+
+template <int L, int W>
+__global__ __launch_bounds__(kLanes * W) void spmm_row_kernel(WaveArgs a, const uint32_t *__restrict__ off,
+                                                             const uint8_t *__restrict__ stream) {
+    constexpr int kRegion = 1024 * L + 16;  // staged values + the decode's 12-byte overread
+    __shared__ __attribute__((aligned(16))) uint8_t regions[W][kRegion];
+    __shared__ __attribute__((aligned(16))) uint8_t luts[W][16 * 8];
+    __shared__ floatx4 parts[W][kLanes];
+    const int lane = threadIdx.x & (kLanes - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kLanes);
+    const int64_t rb = blockIdx.x;
+    const int64_t t0 = wave * a.KT / W, t1 = (wave + 1) * a.KT / W;  // this wavefront's column tiles
+    uint8_t *const region = regions[wave];
+    uint8_t *const lut = luts[wave];
+    if (lane < 16) reinterpret_cast<uint2 *>(lut)[lane] = nibble_selectors((uint32_t)lane);
+    const int n_lane = lane & 15, g4 = 4 * (lane >> 4);
+
+    floatx4 acc[1] = {floatx4{0.f, 0.f, 0.f, 0.f}};
+    if (t0 < t1) {
+        const int64_t n = t1 - t0;
+        const __amdgpu_buffer_rsrc_t xr =
+            __builtin_amdgcn_make_buffer_rsrc((void *)a.X, (short)0, (int)a.x_bytes, kBufferRsrcWord3);
+        // Lanes of tokens >= N start at the resource's end: their loads return zeros.
+        const int xoff = n_lane < a.N ? (int)(n_lane * a.ldx * 2) + 16 * (lane >> 4) : (int)a.x_bytes;
+        const int64_t e0 = rb * a.KT + t0;  // first offset-table entry of the stretch
+        const __amdgpu_buffer_rsrc_t offr = __builtin_amdgcn_make_buffer_rsrc(
+            (void *)(off + e0), (short)0, (int)((n + 1) * 4), kBufferRsrcWord3);
+        const uint32_t offv = __builtin_amdgcn_raw_buffer_load_b32(offr, lane * 4, 0, 0);  // lanes > n: 0
+        WaveRec<L> ring[2];
+        fetch_rec<L>(stream, off[e0], off[e0 + 1], lane, ring[0]);
+        {
+            uint32_t o0 = 0, o1 = 0;  // past the stretch: an empty extent, same load count
+            if (n > 1) {
+                o0 = __builtin_amdgcn_readlane(offv, 1);
+                o1 = __builtin_amdgcn_readlane(offv, 2);
+            }
+            fetch_rec<L>(stream, o0, o1, lane, ring[1]);
+        }
+        v4u32 xb[2][1][kSteps];
+        fetch_x(a, xr, xoff, t0, lane, xb[0][0]);
+        for (int64_t i0 = 0; i0 < n; i0 += 2) {
+#pragma unroll
+            for (int d = 0; d < 2; ++d) {
+                const int64_t i = i0 + d;
+                if (i < n) {
+                    // Stage record i (in-order LDS: the previous decode's reads are done).
+#pragma unroll
+                    for (int k = 0; k < L; ++k) reinterpret_cast<v4u32 *>(region)[lane + kLanes * k] = ring[d].w[k];
+                    const uint2 msk = ring[d].msk;
+                    {
+                        uint32_t o0 = 0, o1 = 0;
+                        if (i + 2 < n) {
+                            o0 = __builtin_amdgcn_readlane(offv, (int)(i + 2));
+                            o1 = __builtin_amdgcn_readlane(offv, (int)(i + 3));
+                        }
+                        fetch_rec<L>(stream, o0, o1, lane, ring[d]);
+                    }
+                    fetch_x(a, xr, xoff, t0 + (i + 1 < n ? i + 1 : i), lane, xb[d ^ 1][0]);
+                    decode_record<1>(as_lds(region), lut, msk, xb[d], acc);
+                }
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0);  // also drains the empty loads past the stretch
+    }
+    parts[wave][lane] = acc[0];
+    __syncthreads();
+    if (wave == 0 && n_lane < a.N) {
+        floatx4 sum = parts[0][lane];
+#pragma unroll
+        for (int w = 1; w < W; ++w) sum += parts[w][lane];  // fixed order: bitwise reproducible
+        store_rows4(a, n_lane, rb * kTileRows + g4, sum);
+    }
+}
+
 // One wavefront per tile: decode every lane-step and store it densely.
 __global__ __launch_bounds__(64) void densify_kernel(const uint8_t *stream, const uint32_t *off, int64_t M,
                                                      int64_t K, int64_t KT, uint16_t *Wd, int64_t ldw) {
@@ -1027,7 +1134,7 @@ static int pass_nt(int64_t N, int64_t n0) {
 // Plans of the single-wavefront kernels (passes of at most 16 tokens).
 // ---------------------------------------------------------------------------
 
-enum WaveKind { kWaveRegs = 0, kWaveDma4 = 1, kWaveNone = 2 };
+enum WaveKind { kWaveRegs = 0, kWaveDma4 = 1, kWaveRow = 2, kWaveNone = 3 };
 
 // Row blocks per unit of the register-staged wave kernel, and the smallest
 // number of units a wavefront streams before a split costs it a partial.
@@ -1047,6 +1154,54 @@ typedef void (*WaveKernelFn)(WaveArgs, const uint32_t *, const uint8_t *);
 // Token blocks of 16 the direct-to-LDS kernel is built for (X for all of them
 // stays in registers): 1 or 2.
 constexpr int kMaxDmaTokenBlocks = 2;
+
+// Wavefronts per workgroup of the row-block kernel: 2, 4, 5 or 8.
+static WaveKernelFn row_kernel(int loads, int wpg) {
+#define USP_ROW(WV)                                   \
+    switch (loads) {                                  \
+        case 2: return spmm_row_kernel<2, WV>;        \
+        case 3: return spmm_row_kernel<3, WV>;        \
+        case 4: return spmm_row_kernel<4, WV>;        \
+        case 5: return spmm_row_kernel<5, WV>;        \
+        case 6: return spmm_row_kernel<6, WV>;        \
+        case 7: return spmm_row_kernel<7, WV>;        \
+        default: return spmm_row_kernel<8, WV>;       \
+    }
+    if (wpg <= 2) {
+        USP_ROW(2)
+    }
+    if (wpg <= 4) {
+        USP_ROW(4)
+    }
+    if (wpg <= 5) {
+        USP_ROW(5)
+    }
+    USP_ROW(8)
+#undef USP_ROW
+}
+
+// Workgroups of the row-block kernel resident per CU.
+static int resident_row_groups(int loads, int wpg) {
+    static int cached[9][9] = {};
+    int &c = cached[loads][wpg];
+    if (c == 0) {
+        int n = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, row_kernel(loads, wpg), kLanes * wpg, 0) != hipSuccess ||
+            n < 1)
+            n = 1;
+        c = n;
+    }
+    return c;
+}
+
+// The most wavefronts per row block (2, 4, 5 or 8, at most KT) for which every
+// row block's workgroup is resident at once.
+static int row_wpg(const usp_matrix *A, int loads) {
+    const int64_t cus = A->num_cus > 0 ? A->num_cus : 256;
+    for (int wpg : {8, 5, 4})
+        if (wpg <= A->KT && A->RB <= cus * resident_row_groups(loads, wpg)) return wpg;
+    return 2;
+}
 
 static WaveKernelFn wave_kernel(WaveKind kind, int loads, int nb) {
 #define USP_BY_LOADS(KERNEL, ...)              \
@@ -1098,12 +1253,14 @@ struct WavePlan {
     bool split;
 };
 
-// Which single-wavefront kernel suits A for N tokens (measured on MI355X):
-// the direct-to-LDS kernel once every wavefront gets at least 8 units of 4
-// row blocks (70B- and 66B-class FFN layers, up to 32 tokens), the
-// register-staged kernel for small matrices and up to 16 tokens (13B attention
-// projections: more, shorter ranges); otherwise the four-wavefront kernel,
-// which shares X through LDS.
+// Which kernel suits A for N tokens (measured on MI355X): the direct-to-LDS
+// kernel once every wavefront gets at least 8 units of 4 row blocks (70B- and
+// 66B-class FFN layers, up to 32 tokens); for small matrices and up to 16
+// tokens, the row-block kernel when there are no more row blocks than CUs (its
+// workgroups then spread evenly) and otherwise the register-staged kernel
+// (13B attention projections: many short single-wavefront ranges balance
+// best); everything else goes to the four-wavefront kernel, which shares X
+// through LDS.
 constexpr int64_t kDmaUnitsPerSlot = 8;
 constexpr int64_t kRegsMaxTiles = 8192;
 static WaveKind wave_kind(const usp_matrix *A, int loads, int64_t N) {
@@ -1112,7 +1269,8 @@ static WaveKind wave_kind(const usp_matrix *A, int loads, int64_t N) {
         const int64_t slots = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(kWaveDma4, loads, nb);
         if (ceil_div(A->RB, kDmaRows) * A->KT >= kDmaUnitsPerSlot * slots) return kWaveDma4;
     }
-    if (nb == 1 && A->RB * A->KT <= kRegsMaxTiles) return kWaveRegs;
+    if (nb == 1 && A->RB * A->KT <= kRegsMaxTiles)
+        return A->RB <= (A->num_cus > 0 ? A->num_cus : 256) ? kWaveRow : kWaveRegs;
     return kWaveNone;
 }
 
@@ -1120,7 +1278,7 @@ static WavePlan plan_wave(const usp_matrix *A, int64_t N) {
     WavePlan p;
     p.loads = wave_loads(A);
     p.kind = wave_kind(A, p.loads, N);
-    if (p.kind == kWaveNone) p.kind = kWaveRegs;  // sizes the workspace for every kernel that may run
+    if (p.kind == kWaveNone || p.kind == kWaveRow) p.kind = kWaveRegs;  // workspace sizing covers every kernel
     p.nb = p.kind == kWaveDma4 ? (int)ceil_div(N, 16) : 1;
     p.rows = p.kind == kWaveDma4 ? kDmaRows : kWaveRows;
     const int64_t min_units = p.kind == kWaveDma4 ? kMinUnitsPerDmaWave : kMinUnitsPerWave;
@@ -1181,8 +1339,30 @@ size_t spmm_workspace_bytes(const usp_matrix *A, int64_t N) {
     return need ? counters_bytes(A) + need : 0;
 }
 
+static int launch_row(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy, int64_t N,
+                      hipStream_t st) {
+    const int loads = wave_loads(A);
+    const int wpg = row_wpg(A, loads);
+    WaveArgs a = {};
+    a.M = A->M;
+    a.K = A->K;
+    a.RB = A->RB;
+    a.KT = A->KT;
+    a.X = reinterpret_cast<const uint16_t *>(X);
+    a.ldx = ldx;
+    a.x_bytes = (uint32_t)(((N - 1) * ldx + A->K) * 2);
+    a.Y = reinterpret_cast<uint16_t *>(Y);
+    a.ldy = ldy;
+    a.N = (int)N;
+    a.y_vec = ((reinterpret_cast<uintptr_t>(Y) & 7) == 0) && (ldy % 4 == 0);
+    hipLaunchKernelGGL(row_kernel(loads, wpg), dim3((unsigned)A->RB), dim3(kLanes * wpg), 0, st, a, A->d_off,
+                       reinterpret_cast<const uint8_t *>(A->d_stream));
+    return (int)hipGetLastError();
+}
+
 static int launch_wave(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy, int64_t N,
                        void *workspace, hipStream_t st) {
+    if (wave_kind(A, wave_loads(A), N) == kWaveRow) return launch_row(A, X, ldx, Y, ldy, N, st);
     const WavePlan p = plan_wave(A, N);
     WaveArgs a;
     a.M = A->M;

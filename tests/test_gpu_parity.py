@@ -266,3 +266,19 @@ def test_every_instance(torch, usp, name):
             res = oracle.check_tolerance(got, Yref, Aref)
             assert res["ok"], (name, s, N, res)
         A.free()
+
+
+# More row blocks than CUs but few tiles: the register-staged kernel with its
+# stream-K split across wavefronts (257 row blocks, the last one ragged; K ends
+# in a partial tile), every output checked.
+def test_register_kernel_exact_full(torch, usp):
+    W, mask, X = wl.make_small_int(4101, 1000, 16, 0.5, seed=25)
+    Y = run(torch, usp, W, mask, X)
+    Yref, _ = oracle.masked_gemm(W, mask, X)
+    assert np.array_equal(Y, Yref)
+
+
+def test_register_kernel_random_full(torch, usp):
+    W, mask, X = wl.make_random(4101, 3000, 13, 0.45, seed=26)
+    Y = run(torch, usp, W, mask, X)
+    assert_close(Y, W, mask, X)
