@@ -488,8 +488,9 @@ struct WaveArgs {
     int64_t ldy;
     int N;
     float *ws;                    // partials [set][slot][token][16 R rows], or null
-    uint32_t *cnt;                // arrival counters per row set (zero between calls)
+    uint32_t *cnt;                // arrival counters per row set and token group (zero between calls)
     int y_vec;
+    int tg;                       // token groups: wavefronts that stream the same units
 };
 
 // Rows m..m+3 of token n (a lane's MFMA outputs), rounded to fp16, those < M.
@@ -509,18 +510,22 @@ __device__ inline void store_rows4(const WaveArgs &a, int n, int64_t m, const fl
     }
 }
 
-// Counts this wavefront's arrival at row set `set` (its partial must already be
-// acknowledged); returns the counter's previous value (in lane 0).
-__device__ inline uint32_t arrive_count(const WaveArgs &a, int64_t set, int lane) {
+// Counts this wavefront's arrival at row set `set` for token group g (its
+// partial must already be acknowledged); returns the counter's previous value
+// (in lane 0).
+__device__ inline uint32_t arrive_count(const WaveArgs &a, int64_t set, int lane, int g = 0) {
     uint32_t old = 0;
-    if (lane == 0) old = __hip_atomic_fetch_add(a.cnt + set, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (lane == 0)
+        old = __hip_atomic_fetch_add(a.cnt + set * a.tg + g, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     return old;
 }
 
 // With the counter's previous value: the last of the nseg arrivals sums every
-// slot in order, stores Y and resets the counter.
+// slot in order for token group g's NB blocks of 16 tokens, stores Y and resets
+// the counter.
 template <int R, int NB = 1>
-__device__ inline void arrive_finish(const WaveArgs &a, int64_t set, int64_t nseg, uint32_t old, int lane) {
+__device__ inline void arrive_finish(const WaveArgs &a, int64_t set, int64_t nseg, uint32_t old, int lane,
+                                     int g = 0) {
     old = __builtin_amdgcn_readfirstlane(old);
     if (old != (uint32_t)nseg - 1u) return;
     const int64_t slot_floats = (int64_t)a.N * kTileRows * R;
@@ -530,7 +535,7 @@ __device__ inline void arrive_finish(const WaveArgs &a, int64_t set, int64_t nse
     const int g4 = 4 * (lane >> 4);
 #pragma unroll 1
     for (int nb = 0; nb < NB; ++nb) {
-        const int n = 16 * nb + (lane & 15);
+        const int n = 16 * (NB * g + nb) + (lane & 15);
         if (n < a.N) {
             // Batches of B slots x R row blocks (16 loads), issued together, then
             // added in slot order per row block: one round trip for up to B slots.
@@ -559,12 +564,12 @@ __device__ inline void arrive_finish(const WaveArgs &a, int64_t set, int64_t nse
             for (int r = 0; r < R; ++r) store_rows4(a, n, (set * R + r) * kTileRows + g4, sum[r]);
         }
     }
-    if (lane == 0) __hip_atomic_store(a.cnt + set, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (lane == 0) __hip_atomic_store(a.cnt + set * a.tg + g, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <int R, int NB = 1>
-__device__ inline void arrive_row_set(const WaveArgs &a, int64_t set, int64_t nseg, int lane) {
-    arrive_finish<R, NB>(a, set, nseg, arrive_count(a, set, lane), lane);
+__device__ inline void arrive_row_set(const WaveArgs &a, int64_t set, int64_t nseg, int lane, int g = 0) {
+    arrive_finish<R, NB>(a, set, nseg, arrive_count(a, set, lane, g), lane, g);
 }
 
 // One tile record in registers: this lane's mask word and L KB of the packed
@@ -762,6 +767,11 @@ __global__ __launch_bounds__(kLanes) void spmm_wave_kernel(WaveArgs a, const uin
 // decoded and no VGPRs hold them. Each slot is its own LDS array: the compiler
 // waits for exactly the transfers into the slot a decode reads. The unit's X
 // operands are loaded into registers one unit ahead.
+// More tokens than one wavefront's registers hold X for are split into token
+// groups: tg wavefronts stream the same units, each for its own NB blocks of 16
+// tokens, and decode every record. Workgroups are dispatched to the eight XCDs
+// in turn, so the group's wavefronts are placed 8 blocks apart: they share one
+// XCD's L2, and the records they all read come from HBM about once.
 // ---------------------------------------------------------------------------
 
 constexpr int kDmaRows = 4;  // row blocks per unit = LDS slots
@@ -811,7 +821,10 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
     __shared__ __attribute__((aligned(16))) uint8_t lut[16 * 8];
     uint8_t *const slots[4] = {slot0, slot1, slot2, slot3};  // indexed by constants < R only
     const int lane = threadIdx.x;
-    const int64_t w = blockIdx.x, G = gridDim.x;
+    // Block b: unit range w of G, token group g (the grid is a multiple of 8 tg).
+    const int64_t b = blockIdx.x, G = gridDim.x / a.tg;
+    const int g = (int)((b >> 3) % a.tg);
+    const int64_t w = (b / (8 * a.tg)) * 8 + (b & 7);
     const int64_t u0 = w * a.units / G, u1 = (w + 1) * a.units / G;
     if (u0 >= u1) return;
     if (lane < 16) reinterpret_cast<uint2 *>(lut)[lane] = nibble_selectors((uint32_t)lane);
@@ -820,10 +833,11 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
         __builtin_amdgcn_make_buffer_rsrc((void *)a.X, (short)0, (int)a.x_bytes, kBufferRsrcWord3);
     const int n_lane = lane & 15, g4 = 4 * (lane >> 4);
     // Lanes of tokens >= N start at the resource's end: their loads return zeros.
+    const int tok0 = 16 * NB * g;  // first token of this wavefront's group
     int xoff[NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-        const int tok = 16 * nb + n_lane;
+        const int tok = tok0 + 16 * nb + n_lane;
         xoff[nb] = tok < a.N ? (int)(tok * a.ldx * 2) + 16 * (lane >> 4) : (int)a.x_bytes;
     }
 
@@ -888,10 +902,10 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
             // answer is read a record or two later, so waiting for it stalls nothing.
             if (r == 1 && pend_set >= 0) {
                 __builtin_amdgcn_s_waitcnt(vmcnt_only(L + 1));
-                old = arrive_count(a, pend_set, lane);
+                old = arrive_count(a, pend_set, lane, g);
             }
             if (r == R - 1 && pend_set >= 0) {
-                arrive_finish<R, NB>(a, pend_set, pend_nseg, old, lane);
+                arrive_finish<R, NB>(a, pend_set, pend_nseg, old, lane, g);
                 pend_set = -1;
             }
             if (r == 0)
@@ -917,7 +931,7 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
             if (w_first == w_last) {
 #pragma unroll
                 for (int nb = 0; nb < NB; ++nb) {
-                    const int tok = 16 * nb + n_lane;
+                    const int tok = tok0 + 16 * nb + n_lane;
                     if (tok < a.N) {
 #pragma unroll
                         for (int r = 0; r < R; ++r) store_rows4(a, tok, (set * R + r) * kTileRows + g4, acc[r][nb]);
@@ -930,7 +944,7 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
                     part_slot, (short)0, (int)(slot_floats * 4), kBufferRsrcWord3);
 #pragma unroll
                 for (int nb = 0; nb < NB; ++nb) {
-                    const int tok = 16 * nb + n_lane;
+                    const int tok = tok0 + 16 * nb + n_lane;
                     if (tok < a.N) {
 #pragma unroll
                         for (int r = 0; r < R; ++r)
@@ -959,7 +973,7 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
         kt = ktn;
     }
     __builtin_amdgcn_s_waitcnt(0);  // also drains the unused prefetches of the range's end
-    if (pend_set >= 0) arrive_row_set<R, NB>(a, pend_set, pend_nseg, lane);
+    if (pend_set >= 0) arrive_row_set<R, NB>(a, pend_set, pend_nseg, lane, g);
 }
 
 // ---------------------------------------------------------------------------
@@ -1151,9 +1165,19 @@ static int wave_loads(const usp_matrix *A) {
 
 typedef void (*WaveKernelFn)(WaveArgs, const uint32_t *, const uint8_t *);
 
-// Token blocks of 16 the direct-to-LDS kernel is built for (X for all of them
-// stays in registers): 1 or 2.
+// Token blocks of 16 a wavefront of the direct-to-LDS kernel serves (X for all
+// of them stays in registers): 1 or 2; and the most token groups (wavefronts
+// streaming the same units for different tokens).
 constexpr int kMaxDmaTokenBlocks = 2;
+constexpr int kMaxDmaTokenGroups = 4;
+constexpr int kMinGroupedTokenBlocks = 4;  // token groups only above this many blocks
+
+// Token blocks per wavefront and token groups of the direct-to-LDS kernel.
+static void dma_tokens(int64_t N, int &nbw, int &tg) {
+    const int nb = (int)ceil_div(N, 16);
+    nbw = nb < kMaxDmaTokenBlocks ? nb : kMaxDmaTokenBlocks;
+    tg = (int)ceil_div(nb, nbw);
+}
 
 // Wavefronts per workgroup of the row-block kernel: 2, 4, 5 or 8.
 static WaveKernelFn row_kernel(int loads, int wpg) {
@@ -1248,14 +1272,14 @@ static int resident_waves(WaveKind kind, int loads, int nb) {
 
 struct WavePlan {
     WaveKind kind;
-    int loads, rows, nb;  // record load groups; row blocks per unit; token blocks
-    int64_t sets, units, grid, maxseg;
+    int loads, rows, nb, tg;  // record load groups; row blocks per unit; token blocks per wavefront; groups
+    int64_t sets, units, ranges, grid, maxseg;  // ranges of units; workgroups = ranges * tg
     bool split;
 };
 
 // Which kernel suits A for N tokens (measured on MI355X): the direct-to-LDS
-// kernel once every wavefront gets at least 8 units of 4 row blocks (70B- and
-// 66B-class FFN layers, up to 32 tokens); for small matrices and up to 16
+// kernel once every range gets at least 8 units of 4 row blocks (70B- and
+// 66B-class FFN layers, up to 128 tokens); for small matrices and up to 16
 // tokens, the row-block kernel when there are no more row blocks than CUs (its
 // workgroups then spread evenly) and otherwise the register-staged kernel
 // (13B attention projections: many short single-wavefront ranges balance
@@ -1265,9 +1289,13 @@ constexpr int64_t kDmaUnitsPerSlot = 8;
 constexpr int64_t kRegsMaxTiles = 8192;
 static WaveKind wave_kind(const usp_matrix *A, int loads, int64_t N) {
     const int nb = (int)ceil_div(N, 16);
-    if (nb <= kMaxDmaTokenBlocks) {
-        const int64_t slots = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(kWaveDma4, loads, nb);
-        if (ceil_div(A->RB, kDmaRows) * A->KT >= kDmaUnitsPerSlot * slots) return kWaveDma4;
+    // Token groups decode every record once per group: measured slower than the
+    // four-wavefront kernel for 3-4 token blocks, faster for 5-8.
+    if (nb <= kMaxDmaTokenBlocks || (nb > kMinGroupedTokenBlocks && nb <= kMaxDmaTokenBlocks * kMaxDmaTokenGroups)) {
+        int nbw, tg;
+        dma_tokens(N, nbw, tg);
+        const int64_t slots = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(kWaveDma4, loads, nbw);
+        if (ceil_div(A->RB, kDmaRows) * A->KT >= kDmaUnitsPerSlot * (slots / tg)) return kWaveDma4;
     }
     if (nb == 1 && A->RB * A->KT <= kRegsMaxTiles)
         return A->RB <= (A->num_cus > 0 ? A->num_cus : 256) ? kWaveRow : kWaveRegs;
@@ -1279,26 +1307,32 @@ static WavePlan plan_wave(const usp_matrix *A, int64_t N) {
     p.loads = wave_loads(A);
     p.kind = wave_kind(A, p.loads, N);
     if (p.kind == kWaveNone || p.kind == kWaveRow) p.kind = kWaveRegs;  // workspace sizing covers every kernel
-    p.nb = p.kind == kWaveDma4 ? (int)ceil_div(N, 16) : 1;
+    p.nb = 1;
+    p.tg = 1;
+    if (p.kind == kWaveDma4) dma_tokens(N, p.nb, p.tg);
     p.rows = p.kind == kWaveDma4 ? kDmaRows : kWaveRows;
     const int64_t min_units = p.kind == kWaveDma4 ? kMinUnitsPerDmaWave : kMinUnitsPerWave;
     p.sets = ceil_div(A->RB, p.rows);
     p.units = p.sets * A->KT;
-    const int64_t slots = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(p.kind, p.loads, p.nb);
+    const int64_t slots =
+        (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(p.kind, p.loads, p.nb) / p.tg;
     const int64_t want = ceil_div(p.units, min_units);
-    p.grid = want < slots ? want : slots;
-    // A range of KT units meets at most ceil(KT / shortest range) + 1 wavefronts.
-    const int64_t shortest = p.units / p.grid;
+    p.ranges = want < slots ? want : slots;
+    if (p.tg > 1) p.ranges = std::max<int64_t>(8, p.ranges / 8 * 8);  // whole groups of 8 ranges x tg
+    p.grid = p.ranges * p.tg;
+    // A range of KT units meets at most ceil(KT / shortest range) + 1 ranges.
+    const int64_t shortest = p.units / p.ranges;
     p.maxseg = ceil_div(A->KT, shortest) + 1;
-    p.split = (p.units % p.grid != 0) || ((p.units / p.grid) % A->KT != 0);
+    p.split = (p.units % p.ranges != 0) || ((p.units / p.ranges) % A->KT != 0);
     return p;
 }
 
-// The wave kernels serve single passes (up to 32 tokens) with X 16-byte
+// The wave kernels serve single passes (up to 128 tokens) with X 16-byte
 // aligned, ldx and K multiples of 8, and X's extent and the offset table
 // addressable by 32-bit offsets.
+constexpr int64_t kMaxWaveTokens = 16 * kMaxDmaTokenBlocks * kMaxDmaTokenGroups;
 static bool use_wave_kernel(const usp_matrix *A, const void *X, int64_t ldx, int64_t N) {
-    if (N > 16 * kMaxDmaTokenBlocks || (reinterpret_cast<uintptr_t>(X) & 15) || ldx % 8 || A->K % 8) return false;
+    if (N > kMaxWaveTokens || (reinterpret_cast<uintptr_t>(X) & 15) || ldx % 8 || A->K % 8) return false;
     const int64_t x_bytes = ((N - 1) * ldx + A->K) * 2;
     if (x_bytes + 2 * A->KT * kTileK >= ((int64_t)1 << 31) || (A->RB * A->KT + 1) * 4 >= ((int64_t)1 << 31))
         return false;
@@ -1310,9 +1344,12 @@ SpmmPlan plan_spmm(const usp_matrix *A, int64_t N) { return plan_pass(A, pass_nt
 // Workspace: one uint32 arrival counter per row group at offset 0 (shared by
 // every pass, zero between passes), padded to 256 bytes, then the fp32 partials
 // of the current pass [row group][slot][tokens][64 rows].
-// Sized for one counter per row block, which also covers one per row group, so
-// every kernel of the library finds zeroed counters at the same place.
-static size_t counters_bytes(const usp_matrix *A) { return ((size_t)A->RB * sizeof(uint32_t) + 255) / 256 * 256; }
+// Sized for one counter per row block (rounded up to whole sets of 4), which
+// also covers one per row group and one per row set and token group (up to 4),
+// so every kernel of the library finds zeroed counters at the same place.
+static size_t counters_bytes(const usp_matrix *A) {
+    return ((size_t)ceil_div(A->RB, kDmaRows) * kDmaRows * sizeof(uint32_t) + 255) / 256 * 256;
+}
 
 static size_t partials_bytes(const SpmmPlan &p, int64_t nb) {
     return (size_t)p.row_groups * (size_t)p.maxseg * (size_t)nb * 64 * sizeof(float);
@@ -1329,7 +1366,7 @@ size_t spmm_workspace_bytes(const usp_matrix *A, int64_t N) {
     // after another and reuse the workspace: full passes of 16 * kMaxNT tokens,
     // then one pass over the remainder; up to 16 tokens may take the wave kernel
     // (sized here too, whichever needs more).
-    size_t need = N <= 16 * kMaxDmaTokenBlocks ? wave_partials_bytes(A, N) : 0;
+    size_t need = N <= kMaxWaveTokens ? wave_partials_bytes(A, N) : 0;
     auto add = [&](int64_t nb) {
         const SpmmPlan p = plan_pass(A, (int)((nb + 15) / 16));
         if (p.split) need = std::max(need, partials_bytes(p, nb));
@@ -1381,6 +1418,7 @@ static int launch_wave(const usp_matrix *A, const void *X, int64_t ldx, void *Y,
     a.cnt = p.split ? reinterpret_cast<uint32_t *>(workspace) : nullptr;
     a.ws = p.split ? reinterpret_cast<float *>(reinterpret_cast<uint8_t *>(workspace) + counters_bytes(A)) : nullptr;
     a.y_vec = ((reinterpret_cast<uintptr_t>(Y) & 7) == 0) && (ldy % 4 == 0);
+    a.tg = p.tg;
     hipLaunchKernelGGL(wave_kernel(p.kind, p.loads, p.nb), dim3((unsigned)p.grid), dim3(kLanes), 0, st, a, A->d_off,
                        reinterpret_cast<const uint8_t *>(A->d_stream));
     return (int)hipGetLastError();

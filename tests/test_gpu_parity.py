@@ -235,6 +235,41 @@ def test_dma_kernel_two_token_blocks_ragged(torch, usp):
     assert_close(Y, W, mask, X)
 
 
+# More than 64 tokens: token groups of the direct-to-LDS kernel (wavefronts
+# streaming the same units, 32 tokens each; 33 to 64 tokens take the
+# four-wavefront kernel). Exact on small integers at 64 and 128 tokens,
+# tolerance at 40 and 100 (the last token block partly past N).
+@pytest.mark.parametrize("N", [64, 128])
+def test_dma_kernel_token_groups_exact(torch, usp, N):
+    W, mask, X = wl.make_small_int(36880, 8088, N, 0.5, seed=27 + N, lo=-1, hi=1)
+    Y = run(torch, usp, W, mask, X)
+    Yref, _ = oracle.masked_gemm(W, mask, X)
+    assert np.array_equal(Y, Yref)
+
+
+@pytest.mark.parametrize("N", [40, 100])
+def test_dma_kernel_token_groups_ragged(torch, usp, N):
+    W, mask, X = wl.make_random(36880, 8088, N, 0.5, seed=28 + N)
+    Y = run(torch, usp, W, mask, X)
+    assert_close(Y, W, mask, X)
+
+
+# 33 to 64 tokens on a matrix whose last row group has one real row block (257
+# row blocks) and whose K ends in a partial tile, every output checked: exact
+# on small integers at 48 tokens, tolerance at 33.
+def test_mid_tokens_ragged_exact(torch, usp):
+    W, mask, X = wl.make_small_int(4101, 1000, 48, 0.5, seed=31)
+    Y = run(torch, usp, W, mask, X)
+    Yref, _ = oracle.masked_gemm(W, mask, X)
+    assert np.array_equal(Y, Yref)
+
+
+def test_mid_tokens_random(torch, usp):
+    W, mask, X = wl.make_random(4101, 3000, 33, 0.45, seed=32)
+    Y = run(torch, usp, W, mask, X)
+    assert_close(Y, W, mask, X)
+
+
 # Every instance of the workload set (6 layers x sparsities x token counts, 38
 # in all), at full size and in the benchmark's launch configuration: the
 # encoding round-trips bit-exactly through the device copy, sampled output rows
