@@ -613,18 +613,23 @@ __device__ inline void fetch_rec(const uint8_t *__restrict__ stream, uint32_t o0
 }
 
 // B operands of one tile: step s, lane (g = lane / 16, n = lane % 16) holds
-// X[n][256 kt + 32 s + 8 g .. + 7]; zero for n >= N (out of the X resource) and
-// for columns >= K.
+// X[n][256 kt + 32 s + 8 g .. + 7]; zero for n >= N and for columns >= K, both
+// by reading at or past the end of the X resource (the hardware returns
+// zeros). Zeroing loaded registers instead would make the compiler wait for
+// the newest loads on that path, and its waits on every path stricter.
 __device__ inline void fetch_x(const WaveArgs &a, __amdgpu_buffer_rsrc_t xr, int xoff, int64_t kt, int lane,
                                v4u32 (&xb)[kSteps]) {
     const int base = xoff + (int)(kt * kTileK * 2);
+    int at[kSteps];
 #pragma unroll
-    for (int s = 0; s < kSteps; ++s) xb[s] = __builtin_amdgcn_raw_buffer_load_b128(xr, base + 64 * s, 0, 0);
+    for (int s = 0; s < kSteps; ++s) at[s] = base + 64 * s;
     if ((kt + 1) * kTileK > a.K) {  // last, partial column tile
 #pragma unroll
         for (int s = 0; s < kSteps; ++s)
-            if (kt * kTileK + 32 * s + 8 * (lane >> 4) >= a.K) xb[s] = v4u32{0u, 0u, 0u, 0u};
+            if (kt * kTileK + 32 * s + 8 * (lane >> 4) >= a.K) at[s] = (int)a.x_bytes;
     }
+#pragma unroll
+    for (int s = 0; s < kSteps; ++s) xb[s] = __builtin_amdgcn_raw_buffer_load_b128(xr, at[s], 0, 0);
 }
 
 // Issue the LDS reads of all 8 steps of a record before expanding any (more
