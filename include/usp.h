@@ -91,6 +91,36 @@ size_t usp_workspace_size(const usp_matrix *A, int64_t N);
 usp_status usp_spmm(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy,
                     int64_t N, void *workspace, size_t ws_bytes, void *stream);
 
+/* Activation of usp_spmm_ex, applied after the bias. */
+typedef enum {
+    USP_ACT_NONE = 0,
+    USP_ACT_RELU = 1,      /* max(v, 0) */
+    USP_ACT_GELU_TANH = 2, /* 0.5 v (1 + tanh(sqrt(2/pi) (v + 0.044715 v^3))) */
+    USP_ACT_SILU = 3       /* v / (1 + exp(-v)) */
+} usp_activation;
+
+/*
+ * usp_spmm_ex -- usp_spmm with a linear layer's epilogue fused into the output
+ * store: Y = act(W X + bias) + residual. The decode-step linear layers the
+ * paper's sparse product replaces (Section 2.1; its models' projections carry a
+ * bias, the FFN an activation, the block a residual add) need nothing else.
+ * Per output, in fp32: the sum, + bias, the activation, + residual, then the
+ * one rounding to fp16 (round to nearest even).
+ *   bias       device fp16 [M] (2-byte aligned), or NULL for none
+ *   residual   device fp16, logical M x N, column n at residual + n * ldr with
+ *              ldr >= M (2-byte aligned), or NULL for none. It may be Y itself
+ *              with ldr == ldy (an in-place add: each output reads its residual
+ *              before it is written, by the same thread); otherwise it must not
+ *              overlap Y.
+ *   activation a usp_activation
+ * Everything else -- arguments, workspace, asynchrony, reproducibility -- as
+ * usp_spmm; usp_spmm(...) equals usp_spmm_ex(..., NULL, NULL, 0, USP_ACT_NONE, ...).
+ * An activation outside usp_activation is USP_ERR_INVALID_ARG.
+ */
+usp_status usp_spmm_ex(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy, int64_t N,
+                       const void *bias, const void *residual, int64_t ldr, int activation,
+                       void *workspace, size_t ws_bytes, void *stream);
+
 /*
  * usp_densify -- writes W with the mask applied (pruned entries as +0) into a
  * dense row-major M x K fp16 device buffer Wd with row stride ldw >= K, by the

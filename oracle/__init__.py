@@ -110,6 +110,46 @@ def masked_bits(W: np.ndarray, mask: np.ndarray, lib=None) -> np.ndarray:
     return out
 
 
+# Fused linear-layer epilogue: Y = act(W X + bias) + residual (float64).
+ACTIVATIONS = {"none": 0, "relu": 1, "gelu_tanh": 2, "silu": 3}
+# Largest slope of each activation (a bound used to carry the product's error
+# through it): 1 for the identity and ReLU; the tanh form of GELU peaks at
+# ~1.129 and SiLU at ~1.100.
+ACT_SLOPE_BOUND = 1.13
+
+
+def activation(v: np.ndarray, act: int) -> np.ndarray:
+    """ReLU: max(v, 0). GELU, tanh form: v/2 * (1 + tanh(sqrt(2/pi) (v + 0.044715 v^3))).
+    SiLU: v / (1 + exp(-v))."""
+    v = np.asarray(v, dtype=np.float64)
+    if act == 0:
+        return v
+    if act == 1:
+        return np.maximum(v, 0.0)
+    if act == 2:
+        return 0.5 * v * (1.0 + np.tanh(np.sqrt(2.0 / np.pi) * (v + 0.044715 * v ** 3)))
+    if act == 3:
+        with np.errstate(over="ignore"):
+            return v / (1.0 + np.exp(-v))
+    raise ValueError(f"unknown activation {act}")
+
+
+def linear_epilogue(Yref: np.ndarray, A: np.ndarray, act: int, bias=None, residual=None):
+    """The product's reference (Yref, A of shape (N, R)) through the epilogue:
+    Y = act(Yref + bias) + residual, and the scale its error is bounded by,
+    A' = L (A + |bias|) + |residual| (L = 1 without an activation's slope).
+    bias: float64 [R] or None; residual: float64 (N, R) or None."""
+    z = Yref + (0.0 if bias is None else bias[None, :])
+    y = activation(z, act)
+    scale = A + (0.0 if bias is None else np.abs(bias)[None, :])
+    if act in (2, 3):
+        scale = ACT_SLOPE_BOUND * scale
+    if residual is not None:
+        y = y + residual
+        scale = scale + np.abs(residual)
+    return y, scale
+
+
 def num_threads(lib=None) -> int:
     return int((lib or load()).oracle_num_threads())
 

@@ -104,26 +104,49 @@ size_t usp_workspace_size(const usp_matrix *A, int64_t N) {
     return usp::spmm_workspace_bytes(A, N);
 }
 
-usp_status usp_spmm(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy, int64_t N,
-                    void *workspace, size_t ws_bytes, void *stream) {
-    if (!alive(A)) return usp::fail(USP_ERR_INVALID_ARG, "usp_spmm: invalid or freed handle");
-    if (!X || !Y) return usp::fail(USP_ERR_INVALID_ARG, "usp_spmm: null X or Y");
-    if (N < 1) return usp::fail(USP_ERR_INVALID_ARG, "usp_spmm: N must be >= 1");
-    if (N > (int64_t)1 << 20) return usp::fail(USP_ERR_UNSUPPORTED, "usp_spmm: N too large");
-    if (ldx < A->K) return usp::fail(USP_ERR_INVALID_ARG, "usp_spmm: ldx must be >= K");
-    if (ldy < A->M) return usp::fail(USP_ERR_INVALID_ARG, "usp_spmm: ldy must be >= M");
+static usp_status spmm_common(const char *fn, const usp_matrix *A, const void *X, int64_t ldx, void *Y,
+                              int64_t ldy, int64_t N, const usp::Epilogue &ep, void *workspace, size_t ws_bytes,
+                              void *stream) {
+    const std::string f(fn);
+    if (!alive(A)) return usp::fail(USP_ERR_INVALID_ARG, f + ": invalid or freed handle");
+    if (!X || !Y) return usp::fail(USP_ERR_INVALID_ARG, f + ": null X or Y");
+    if (N < 1) return usp::fail(USP_ERR_INVALID_ARG, f + ": N must be >= 1");
+    if (N > (int64_t)1 << 20) return usp::fail(USP_ERR_UNSUPPORTED, f + ": N too large");
+    if (ldx < A->K) return usp::fail(USP_ERR_INVALID_ARG, f + ": ldx must be >= K");
+    if (ldy < A->M) return usp::fail(USP_ERR_INVALID_ARG, f + ": ldy must be >= M");
     if ((reinterpret_cast<uintptr_t>(X) & 1) || (reinterpret_cast<uintptr_t>(Y) & 1))
-        return usp::fail(USP_ERR_INVALID_ARG, "usp_spmm: X and Y must be 2-byte aligned");
+        return usp::fail(USP_ERR_INVALID_ARG, f + ": X and Y must be 2-byte aligned");
+    if (ep.act < USP_ACT_NONE || ep.act > USP_ACT_SILU)
+        return usp::fail(USP_ERR_INVALID_ARG, f + ": unknown activation");
+    if (reinterpret_cast<uintptr_t>(ep.bias) & 1) return usp::fail(USP_ERR_INVALID_ARG, f + ": bias must be 2-byte aligned");
+    if (ep.res && ((reinterpret_cast<uintptr_t>(ep.res) & 1) || ep.ldr < A->M))
+        return usp::fail(USP_ERR_INVALID_ARG, f + ": residual must be 2-byte aligned with ldr >= M");
     const size_t need = usp::spmm_workspace_bytes(A, N);
     if (need && (!workspace || ws_bytes < need))
-        return usp::fail(USP_ERR_INVALID_ARG, "usp_spmm: workspace too small (see usp_workspace_size)");
+        return usp::fail(USP_ERR_INVALID_ARG, f + ": workspace too small (see usp_workspace_size)");
     if (need && (reinterpret_cast<uintptr_t>(workspace) & 15))
-        return usp::fail(USP_ERR_INVALID_ARG, "usp_spmm: workspace must be 16-byte aligned");
+        return usp::fail(USP_ERR_INVALID_ARG, f + ": workspace must be 16-byte aligned");
     DeviceGuard g(A->device);
-    if (!g.ok) return usp::fail(USP_ERR_HIP, "usp_spmm: cannot select device");
-    const int rc = usp::launch_spmm(A, X, ldx, Y, ldy, N, workspace, stream);
-    if (rc != 0) return hip_fail((hipError_t)rc, "usp_spmm: launch");
+    if (!g.ok) return usp::fail(USP_ERR_HIP, f + ": cannot select device");
+    const int rc = usp::launch_spmm(A, X, ldx, Y, ldy, N, ep, workspace, stream);
+    if (rc != 0) return hip_fail((hipError_t)rc, (f + ": launch").c_str());
     return USP_OK;
+}
+
+usp_status usp_spmm(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy, int64_t N,
+                    void *workspace, size_t ws_bytes, void *stream) {
+    return spmm_common("usp_spmm", A, X, ldx, Y, ldy, N, usp::Epilogue(), workspace, ws_bytes, stream);
+}
+
+usp_status usp_spmm_ex(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy, int64_t N,
+                       const void *bias, const void *residual, int64_t ldr, int activation, void *workspace,
+                       size_t ws_bytes, void *stream) {
+    usp::Epilogue ep;
+    ep.bias = reinterpret_cast<const uint16_t *>(bias);
+    ep.res = reinterpret_cast<const uint16_t *>(residual);
+    ep.ldr = ldr;
+    ep.act = activation;
+    return spmm_common("usp_spmm_ex", A, X, ldx, Y, ldy, N, ep, workspace, ws_bytes, stream);
 }
 
 usp_status usp_densify(const usp_matrix *A, void *Wd, int64_t ldw, void *stream) {

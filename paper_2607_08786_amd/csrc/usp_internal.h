@@ -53,8 +53,15 @@ struct SpmmPlan {
 };
 SpmmPlan plan_spmm(const usp_matrix *A, int64_t N);
 size_t spmm_workspace_bytes(const usp_matrix *A, int64_t N);
+// Fused output epilogue: Y = act(W X + bias) + residual (all optional).
+struct Epilogue {
+    const uint16_t *bias = nullptr;  // fp16 [M]
+    const uint16_t *res = nullptr;   // fp16, column n at res + n * ldr
+    int64_t ldr = 0;
+    int act = 0;                     // usp_activation
+};
 int launch_spmm(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy, int64_t N,
-                void *workspace, void *stream);
+                const Epilogue &ep, void *workspace, void *stream);
 int launch_densify(const usp_matrix *A, void *Wd, int64_t ldw, void *stream);
 
 }  // namespace usp

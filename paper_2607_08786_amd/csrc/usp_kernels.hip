@@ -71,7 +71,27 @@ struct SpmmArgs {
     uint32_t *cnt;    // arrival counters, one per row group (zero between calls)
     int x_vec;        // X chunks may be read as 16-byte vectors
     int y_vec;        // Y may be written as 8-byte vectors
+    const uint16_t *bias;  // fused epilogue (Epilogue): fp16 [M] or null
+    const uint16_t *res;   // fp16 residual, token n at res + n * ldr, or null
+    int64_t ldr;
+    int act;               // usp_activation
 };
+
+// The fused epilogue of one output (row m, token n), in fp32: + bias, the
+// activation, + residual. Arguments are uniform, so the branches are too.
+template <class Args>
+__device__ inline float epilogue(const Args &a, int n, int64_t m, float v) {
+    if (a.bias) v += (float)__builtin_bit_cast(_Float16, a.bias[m]);
+    if (a.act == 1) {
+        v = v > 0.f ? v : 0.f;
+    } else if (a.act == 2) {  // tanh form of GELU; sqrt(2 / pi) = 0.7978845608...
+        v = 0.5f * v * (1.f + tanhf(0.7978845608028654f * (v + 0.044715f * v * v * v)));
+    } else if (a.act == 3) {
+        v = v / (1.f + expf(-v));
+    }
+    if (a.res) v += (float)__builtin_bit_cast(_Float16, a.res[(int64_t)n * a.ldr + m]);
+    return v;
+}
 
 // Selector pair for expanding nibble `n` (positions 0..3) from the 4 packed
 // halfs (c0,c1 | c2,c3) held in x0 | x1: output half j takes c_rank(j) when bit
@@ -237,8 +257,15 @@ __device__ inline uint4 load_x_chunk(const SpmmArgs &a, int n, int64_t k) {
     return v;
 }
 
-// Rounds four consecutive rows m..m+3 of token n to fp16 and stores those < M.
+// Rounds four consecutive rows m..m+3 of token n to fp16 (after the fused
+// epilogue, if any) and stores those < M.
 __device__ inline void store_y4(const SpmmArgs &a, int n, int64_t m, float v0, float v1, float v2, float v3) {
+    if (a.bias || a.res || a.act) {
+        if (m < a.M) v0 = epilogue(a, n, m, v0);
+        if (m + 1 < a.M) v1 = epilogue(a, n, m + 1, v1);
+        if (m + 2 < a.M) v2 = epilogue(a, n, m + 2, v2);
+        if (m + 3 < a.M) v3 = epilogue(a, n, m + 3, v3);
+    }
     const uint16_t h0 = __builtin_bit_cast(uint16_t, (_Float16)v0);
     const uint16_t h1 = __builtin_bit_cast(uint16_t, (_Float16)v1);
     const uint16_t h2 = __builtin_bit_cast(uint16_t, (_Float16)v2);
@@ -491,10 +518,21 @@ struct WaveArgs {
     uint32_t *cnt;                // arrival counters per row set and token group (zero between calls)
     int y_vec;
     int tg;                       // token groups: wavefronts that stream the same units
+    const uint16_t *bias;         // fused epilogue (Epilogue): fp16 [M] or null
+    const uint16_t *res;          // fp16 residual, token n at res + n * ldr, or null
+    int64_t ldr;
+    int act;                      // usp_activation
 };
 
-// Rows m..m+3 of token n (a lane's MFMA outputs), rounded to fp16, those < M.
-__device__ inline void store_rows4(const WaveArgs &a, int n, int64_t m, const floatx4 &v) {
+// Rows m..m+3 of token n (a lane's MFMA outputs), rounded to fp16 after the
+// fused epilogue (if any), those < M.
+__device__ inline void store_rows4(const WaveArgs &a, int n, int64_t m, const floatx4 &acc) {
+    floatx4 v = acc;
+    if (a.bias || a.res || a.act) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            if (m + i < a.M) v[i] = epilogue(a, n, m + i, v[i]);
+    }
     const uint16_t h0 = __builtin_bit_cast(uint16_t, (_Float16)v[0]);
     const uint16_t h1 = __builtin_bit_cast(uint16_t, (_Float16)v[1]);
     const uint16_t h2 = __builtin_bit_cast(uint16_t, (_Float16)v[2]);
@@ -1381,8 +1419,15 @@ size_t spmm_workspace_bytes(const usp_matrix *A, int64_t N) {
     return need ? counters_bytes(A) + need : 0;
 }
 
+static void set_epilogue(WaveArgs &a, const Epilogue &ep) {
+    a.bias = ep.bias;
+    a.res = ep.res;
+    a.ldr = ep.ldr;
+    a.act = ep.act;
+}
+
 static int launch_row(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy, int64_t N,
-                      hipStream_t st) {
+                      const Epilogue &ep, hipStream_t st) {
     const int loads = wave_loads(A);
     const int wpg = row_wpg(A, loads);
     WaveArgs a = {};
@@ -1397,14 +1442,15 @@ static int launch_row(const usp_matrix *A, const void *X, int64_t ldx, void *Y, 
     a.ldy = ldy;
     a.N = (int)N;
     a.y_vec = ((reinterpret_cast<uintptr_t>(Y) & 7) == 0) && (ldy % 4 == 0);
+    set_epilogue(a, ep);
     hipLaunchKernelGGL(row_kernel(loads, wpg), dim3((unsigned)A->RB), dim3(kLanes * wpg), 0, st, a, A->d_off,
                        reinterpret_cast<const uint8_t *>(A->d_stream));
     return (int)hipGetLastError();
 }
 
 static int launch_wave(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy, int64_t N,
-                       void *workspace, hipStream_t st) {
-    if (wave_kind(A, wave_loads(A), N) == kWaveRow) return launch_row(A, X, ldx, Y, ldy, N, st);
+                       const Epilogue &ep, void *workspace, hipStream_t st) {
+    if (wave_kind(A, wave_loads(A), N) == kWaveRow) return launch_row(A, X, ldx, Y, ldy, N, ep, st);
     const WavePlan p = plan_wave(A, N);
     WaveArgs a;
     a.M = A->M;
@@ -1424,15 +1470,16 @@ static int launch_wave(const usp_matrix *A, const void *X, int64_t ldx, void *Y,
     a.ws = p.split ? reinterpret_cast<float *>(reinterpret_cast<uint8_t *>(workspace) + counters_bytes(A)) : nullptr;
     a.y_vec = ((reinterpret_cast<uintptr_t>(Y) & 7) == 0) && (ldy % 4 == 0);
     a.tg = p.tg;
+    set_epilogue(a, ep);
     hipLaunchKernelGGL(wave_kernel(p.kind, p.loads, p.nb), dim3((unsigned)p.grid), dim3(kLanes), 0, st, a, A->d_off,
                        reinterpret_cast<const uint8_t *>(A->d_stream));
     return (int)hipGetLastError();
 }
 
 int launch_spmm(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy, int64_t N,
-                void *workspace, void *stream) {
+                const Epilogue &ep, void *workspace, void *stream) {
     hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-    if (use_wave_kernel(A, X, ldx, N)) return launch_wave(A, X, ldx, Y, ldy, N, workspace, st);
+    if (use_wave_kernel(A, X, ldx, N)) return launch_wave(A, X, ldx, Y, ldy, N, ep, workspace, st);
     for (int64_t n0 = 0; n0 < N; n0 += 16 * kMaxNT) {
         const int nb = (int)((N - n0) < 16 * kMaxNT ? (N - n0) : 16 * kMaxNT);
         const int nt = (nb + 15) / 16;
@@ -1457,6 +1504,10 @@ int launch_spmm(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_
         a.cnt = ws ? reinterpret_cast<uint32_t *>(workspace) : nullptr;
         a.x_vec = ((reinterpret_cast<uintptr_t>(a.X) & 15) == 0) && (ldx % 8 == 0);
         a.y_vec = ((reinterpret_cast<uintptr_t>(a.Y) & 7) == 0) && (ldy % 4 == 0);
+        a.bias = ep.bias;
+        a.res = ep.res ? ep.res + n0 * ep.ldr : nullptr;
+        a.ldr = ep.ldr;
+        a.act = ep.act;
         const dim3 grid((unsigned)p.grid), block(kThreads);
         const bool xfast = a.x_vec && (A->K % 8 == 0);
 #define USP_LAUNCH(NTV)                                                                              \

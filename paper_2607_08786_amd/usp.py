@@ -20,8 +20,11 @@ USP_OK = 0
 _STATUS = {0: "USP_OK", 1: "USP_ERR_INVALID_ARG", 2: "USP_ERR_UNSUPPORTED", 3: "USP_ERR_OOM",
            4: "USP_ERR_HIP", 5: "USP_ERR_INTERNAL"}
 
-EXPORTED = ("usp_encode", "usp_workspace_size", "usp_spmm", "usp_densify", "usp_decode",
+EXPORTED = ("usp_encode", "usp_workspace_size", "usp_spmm", "usp_spmm_ex", "usp_densify", "usp_decode",
             "usp_info", "usp_free", "usp_last_error")
+
+# usp_activation
+ACTIVATIONS = {"none": 0, "relu": 1, "gelu_tanh": 2, "silu": 3}
 
 
 class UspError(RuntimeError):
@@ -57,6 +60,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.usp_workspace_size.restype = sz
     lib.usp_spmm.argtypes = [p, p, i64, p, i64, i64, p, sz, p]
     lib.usp_spmm.restype = st
+    lib.usp_spmm_ex.argtypes = [p, p, i64, p, i64, i64, p, p, i64, ctypes.c_int, p, sz, p]
+    lib.usp_spmm_ex.restype = st
     lib.usp_densify.argtypes = [p, p, i64, p]
     lib.usp_densify.restype = st
     lib.usp_decode.argtypes = [p, p, p]
@@ -128,6 +133,37 @@ def usp_spmm(handle: int, X: torch.Tensor, Y: torch.Tensor, workspace: torch.Ten
                                    ws_ptr, ws_bytes, _stream_handle(stream)))
 
 
+def usp_spmm_ex(handle: int, X: torch.Tensor, Y: torch.Tensor, workspace: torch.Tensor | None = None,
+                bias: torch.Tensor | None = None, residual: torch.Tensor | None = None,
+                activation: str | int = "none", stream=None) -> None:
+    """Y = act(X @ W^T + bias) + residual (token-major fp16 device tensors; bias [M],
+    residual [N, M] with unit inner stride, or None; residual may be Y itself)."""
+    if X.dtype != torch.float16 or Y.dtype != torch.float16:
+        raise TypeError("X and Y must be float16")
+    if X.dim() != 2 or Y.dim() != 2 or X.stride(1) != 1 or Y.stride(1) != 1:
+        raise TypeError("X and Y must be 2-D with unit inner stride")
+    N = X.shape[0]
+    if Y.shape[0] != N:
+        raise ValueError("X and Y must have the same number of tokens")
+    act = ACTIVATIONS[activation] if isinstance(activation, str) else int(activation)
+    b_ptr = r_ptr = None
+    ldr = 0
+    if bias is not None:
+        if bias.dtype != torch.float16 or bias.dim() != 1 or bias.stride(0) != 1 or bias.shape[0] != Y.shape[1]:
+            raise TypeError("bias must be a contiguous float16 vector of M entries")
+        b_ptr = bias.data_ptr()
+    if residual is not None:
+        if residual.dtype != torch.float16 or residual.dim() != 2 or residual.stride(1) != 1 \
+                or tuple(residual.shape) != tuple(Y.shape):
+            raise TypeError("residual must be a float16 [N, M] tensor with unit inner stride")
+        r_ptr, ldr = residual.data_ptr(), residual.stride(0)
+    ws_ptr, ws_bytes = None, 0
+    if workspace is not None:
+        ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
+    _check(load_library().usp_spmm_ex(handle, X.data_ptr(), X.stride(0), Y.data_ptr(), Y.stride(0), N,
+                                      b_ptr, r_ptr, ldr, act, ws_ptr, ws_bytes, _stream_handle(stream)))
+
+
 def usp_densify(handle: int, Wd: torch.Tensor, stream=None) -> None:
     if Wd.dtype != torch.float16 or Wd.dim() != 2 or Wd.stride(1) != 1:
         raise TypeError("Wd must be a 2-D float16 tensor with unit inner stride")
@@ -172,13 +208,19 @@ class SparseMatrix:
             return None
         return torch.zeros(n, dtype=torch.uint8, device=f"cuda:{self.device}")  # zeroed once
 
-    def spmm(self, X: torch.Tensor, Y: torch.Tensor | None = None, workspace=None, stream=None) -> torch.Tensor:
+    def spmm(self, X: torch.Tensor, Y: torch.Tensor | None = None, workspace=None, stream=None,
+             bias: torch.Tensor | None = None, residual: torch.Tensor | None = None,
+             activation: str | int = "none") -> torch.Tensor:
+        """Y = W X (token-major), or act(W X + bias) + residual when any of those is given."""
         N = X.shape[0]
         if Y is None:
             Y = torch.empty((N, self.M), dtype=torch.float16, device=X.device)
         if workspace is None:
             workspace = self.make_workspace(N)
-        usp_spmm(self.handle, X, Y, workspace, stream)
+        if bias is None and residual is None and activation in ("none", 0):
+            usp_spmm(self.handle, X, Y, workspace, stream)
+        else:
+            usp_spmm_ex(self.handle, X, Y, workspace, bias, residual, activation, stream)
         return Y
 
     def densify(self, stream=None) -> torch.Tensor:

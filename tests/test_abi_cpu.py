@@ -65,3 +65,15 @@ def test_last_error_is_thread_local(usp):
     t.start()
     t.join()
     assert seen == [""]
+
+
+def test_sparse_linear_op_is_registered():
+    # The custom operator exists and its fake (meta) implementation gives the
+    # output shape without a device.
+    import torch
+    from torch._subclasses.fake_tensor import FakeTensorMode
+    import paper_2607_08786_amd.linear  # noqa: F401
+    with FakeTensorMode():
+        x = torch.empty(7, 64, dtype=torch.float16)
+        y = torch.ops.usp.sparse_linear(x, 0, 33, None, None, 1, None)
+    assert tuple(y.shape) == (7, 33) and y.dtype == torch.float16

@@ -270,6 +270,90 @@ def test_mid_tokens_random(torch, usp):
     assert_close(Y, W, mask, X)
 
 
+# Fused epilogue (usp_spmm_ex): Y = act(W X + bias) + residual against the
+# oracle's product through the same epilogue, with the error scale carried
+# through the activation's largest slope. Every kernel: the row-block kernel
+# (1024 x 1024, 16 tokens), the register-staged kernel (4101 x 1000, 16), the
+# four-wavefront kernel (48 tokens), the direct-to-LDS kernel (36880 x 8088:
+# 16 tokens, 27 tokens, 100 tokens in token groups).
+EPI_SMALL = [(1024, 1024, 16), (4101, 1000, 16), (4101, 1000, 48)]
+EPI_LARGE = [((36880, 8088, 16), "gelu_tanh"), ((36880, 8088, 27), "silu"), ((36880, 8088, 100), "relu")]
+
+
+def _epilogue_case(torch, usp, M, K, N, act, seed, rows=None, inplace=False, use_bias=True, use_res=True):
+    W, mask, X = wl.make_random(M, K, N, 0.5, seed=seed)
+    rng = np.random.default_rng(seed + 1)
+    bias = rng.normal(0, 0.5, M).astype(np.float16).view(np.uint16)
+    res = rng.normal(0, 1.0, (N, M)).astype(np.float16).view(np.uint16)
+    A = usp.SparseMatrix(W, mask)
+    Xd = to_dev(torch, X)
+    bd = to_dev(torch, bias) if use_bias else None
+    rd = to_dev(torch, res) if use_res else None
+    if inplace:
+        Y = rd.clone()
+        A.spmm(Xd, Y=Y, bias=bd, residual=Y, activation=act)
+    else:
+        Y = A.spmm(Xd, bias=bd, residual=rd, activation=act)
+    torch.cuda.synchronize()
+    A.free()
+    got = Y.cpu().numpy().astype(np.float64)
+    Yref, Aref = oracle.masked_gemm(W, mask, X, rows=rows)
+    cols = np.arange(M) if rows is None else rows
+    got = got[:, cols]
+    b64 = oracle.f16_to_f64(bias)[cols] if use_bias else None
+    r64 = oracle.f16_to_f64(res)[:, cols] if use_res else None
+    y, scale = oracle.linear_epilogue(Yref, Aref, oracle.ACTIVATIONS[act], bias=b64, residual=r64)
+    out = oracle.check_tolerance(got, y, scale)
+    assert out["ok"], (M, K, N, act, out)
+
+
+@pytest.mark.parametrize("shape", EPI_SMALL)
+@pytest.mark.parametrize("act", ["none", "relu", "gelu_tanh", "silu"])
+def test_fused_epilogue_small(torch, usp, shape, act):
+    M, K, N = shape
+    _epilogue_case(torch, usp, M, K, N, act, seed=40 + M % 7 + N)
+
+
+@pytest.mark.parametrize("case", EPI_LARGE)
+def test_fused_epilogue_large(torch, usp, case):
+    (M, K, N), act = case
+    rows = np.sort(np.unique(np.concatenate([np.random.default_rng(2).choice(M, 200, replace=False),
+                                             [0, 15, 16, M - 16, M - 1]])))
+    _epilogue_case(torch, usp, M, K, N, act, seed=50 + N, rows=rows)
+
+
+def test_fused_epilogue_inplace_residual_and_parts(torch, usp):
+    # Residual read from Y itself (in-place add); bias alone; residual alone.
+    _epilogue_case(torch, usp, 4101, 1000, 16, "silu", seed=61, inplace=True)
+    _epilogue_case(torch, usp, 4101, 1000, 48, "gelu_tanh", seed=62, inplace=True)
+    _epilogue_case(torch, usp, 1024, 1024, 16, "none", seed=63, use_res=False)
+    _epilogue_case(torch, usp, 4101, 1000, 16, "none", seed=64, use_bias=False)
+
+
+def test_sparse_linear_module(torch, usp):
+    # The nn.Linear drop-in: 3-D input (2 x 8 tokens), fused ReLU and residual.
+    from paper_2607_08786_amd.linear import SparseLinear
+    torch.manual_seed(0)
+    lin = torch.nn.Linear(1000, 4101).to("cuda", torch.float16)
+    rng = np.random.default_rng(7)
+    mask = (rng.random((4101, 1000)) < 0.5).astype(np.uint8)
+    mod = SparseLinear.from_linear(lin, mask, activation="relu")
+    x = torch.randn(2, 8, 1000, device="cuda", dtype=torch.float16)
+    r = torch.randn(2, 8, 4101, device="cuda", dtype=torch.float16)
+    y = mod(x, residual=r)
+    y2 = mod(x, residual=r)
+    torch.cuda.synchronize()
+    assert y.shape == (2, 8, 4101) and torch.equal(y, y2)
+    W = lin.weight.detach().cpu().numpy().view(np.uint16)
+    X = x.reshape(16, 1000).cpu().numpy().view(np.uint16)
+    Yref, Aref = oracle.masked_gemm(W, mask, X)
+    b64 = oracle.f16_to_f64(lin.bias.detach().cpu().numpy().view(np.uint16))
+    r64 = oracle.f16_to_f64(r.reshape(16, 4101).cpu().numpy().view(np.uint16))
+    yref, scale = oracle.linear_epilogue(Yref, Aref, 1, bias=b64, residual=r64)
+    out = oracle.check_tolerance(y.reshape(16, 4101).cpu().numpy().astype(np.float64), yref, scale)
+    assert out["ok"], out
+
+
 # Every instance of the workload set (6 layers x sparsities x token counts, 38
 # in all), at full size and in the benchmark's launch configuration: the
 # encoding round-trips bit-exactly through the device copy, sampled output rows

@@ -29,3 +29,43 @@ def test_pins_catch_planted_mistake(tmp_path, mutant):
         except AssertionError:
             caught.append(pin.__name__)
     assert caught, f"no pin caught planted mistake {mutant}"
+
+
+# --- fused epilogue (activations) -----------------------------------------
+
+def test_activations_pinned():
+    import math
+
+    import numpy as np
+    from scipy.special import expit
+    x = np.linspace(-12.0, 12.0, 4801)
+    relu, gelu, silu = (oracle.activation(x, a) for a in (1, 2, 3))
+    # Odd-part identities: f(x) - f(-x) = x for ReLU, both GELU forms and SiLU.
+    for f, a in ((relu, 1), (gelu, 2), (silu, 3)):
+        assert np.allclose(f - oracle.activation(-x, a), x, rtol=0, atol=1e-12)
+    assert np.array_equal(relu, np.where(x > 0, x, 0.0))
+    # SiLU = x * logistic(x) (scipy's logistic function).
+    assert np.allclose(silu, x * expit(x), rtol=1e-14, atol=1e-300)
+    # The tanh form of GELU stays within 1e-3 of the exact GELU x * Phi(x).
+    exact = np.array([0.5 * v * (1.0 + math.erf(v / math.sqrt(2.0))) for v in x])
+    assert np.max(np.abs(gelu - exact)) < 1e-3
+    # Slopes: 1/2 at 0 for GELU and SiLU; never above the bound the tolerance uses.
+    h = 1e-6
+    for a in (2, 3):
+        d0 = (oracle.activation(np.array([h]), a) - oracle.activation(np.array([-h]), a))[0] / (2 * h)
+        assert abs(d0 - 0.5) < 1e-6
+        slope = np.diff(oracle.activation(x, a)) / np.diff(x)
+        assert slope.max() < oracle.ACT_SLOPE_BOUND and slope.max() > 1.05
+
+
+def test_linear_epilogue_scale():
+    import numpy as np
+    rng = np.random.default_rng(4)
+    Y = rng.normal(size=(3, 5)); A = np.abs(Y) + 1.0
+    b = rng.normal(size=5); r = rng.normal(size=(3, 5))
+    y0, s0 = oracle.linear_epilogue(Y, A, 0)
+    assert np.array_equal(y0, Y) and np.array_equal(s0, A)
+    y1, s1 = oracle.linear_epilogue(Y, A, 1, bias=b, residual=r)
+    assert np.allclose(y1, np.maximum(Y + b, 0) + r) and np.allclose(s1, A + np.abs(b) + np.abs(r))
+    _, s3 = oracle.linear_epilogue(Y, A, 3, bias=b)
+    assert np.allclose(s3, oracle.ACT_SLOPE_BOUND * (A + np.abs(b)))
