@@ -82,7 +82,8 @@ size_t usp_workspace_size(const usp_matrix *A, int64_t N);
  *       bytes (may be NULL when that size is 0); owned by the caller; must not be
  *       used by another in-flight call. It must be zero-filled before its first
  *       use; every completed call leaves it ready for the next one (with any
- *       handle and any N), so it is cleared once, not per call.
+ *       handle of up to 2^20 rows and any N), so it is cleared once, not per
+ *       call. A handle with more rows needs a workspace of its own.
  * Accumulation is fp32 in a fixed order: results are bitwise reproducible run
  * to run. The output is rounded to fp16 with round-to-nearest-even.
  * Inputs with X not 16-byte aligned or ldx not a multiple of 8 take a slower

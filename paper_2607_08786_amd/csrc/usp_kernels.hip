@@ -1387,11 +1387,16 @@ SpmmPlan plan_spmm(const usp_matrix *A, int64_t N) { return plan_pass(A, pass_nt
 // Workspace: one uint32 arrival counter per row group at offset 0 (shared by
 // every pass, zero between passes), padded to 256 bytes, then the fp32 partials
 // of the current pass [row group][slot][tokens][64 rows].
-// Sized for one counter per row block (rounded up to whole sets of 4), which
-// also covers one per row group and one per row set and token group (up to 4),
-// so every kernel of the library finds zeroed counters at the same place.
+// The counters take the first kCounterRegionBytes of every workspace whatever
+// the handle (one per row block, rounded up to whole sets of 4, fits for up to
+// 2^20 rows; also one per row group and one per row set and token group), and
+// the partials start after it: partials a call leaves behind never sit where
+// another handle's counters are, so one zero-filled workspace serves calls with
+// any handle and any N. Larger handles need a workspace of their own.
+constexpr size_t kCounterRegionBytes = 256 * 1024;
 static size_t counters_bytes(const usp_matrix *A) {
-    return ((size_t)ceil_div(A->RB, kDmaRows) * kDmaRows * sizeof(uint32_t) + 255) / 256 * 256;
+    const size_t need = ((size_t)ceil_div(A->RB, kDmaRows) * kDmaRows * sizeof(uint32_t) + 255) / 256 * 256;
+    return need > kCounterRegionBytes ? need : kCounterRegionBytes;
 }
 
 static size_t partials_bytes(const SpmmPlan &p, int64_t nb) {

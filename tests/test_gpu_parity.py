@@ -183,6 +183,29 @@ def test_workspace_contract(torch, usp):
     A.free()
 
 
+# One zero-filled workspace shared by handles of different sizes, calls
+# alternating: partials a call leaves behind must never be read as another
+# handle's arrival counters (4101 x 3000 splits its row blocks through the
+# register-staged kernel, 36880 x 8088 through the direct-to-LDS kernel, and
+# 4101 x 1000 at 48 tokens through the four-wavefront kernel). Exact small
+# integers, every output.
+def test_workspace_shared_between_handles(torch, usp):
+    cases = [wl.make_small_int(4101, 3000, 16, 0.5, seed=71, lo=-1, hi=1),
+             wl.make_small_int(36880, 8088, 16, 0.5, seed=72, lo=-1, hi=1),
+             wl.make_small_int(4101, 1000, 48, 0.5, seed=73, lo=-1, hi=1)]
+    mats = [usp.SparseMatrix(W, m) for W, m, _ in cases]
+    need = max(A.workspace_size(X.shape[0]) for A, (_, _, X) in zip(mats, cases))
+    ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
+    refs = [oracle.masked_gemm(W, m, X)[0] for W, m, X in cases]
+    for it in range(2):
+        for A, (W, m, X), Yref in zip(mats, cases, refs):
+            Y = A.spmm(to_dev(torch, X), workspace=ws)
+            torch.cuda.synchronize()
+            assert np.array_equal(Y.cpu().numpy().astype(np.float64), Yref), (it, A.M, A.K, X.shape[0])
+    for A in mats:
+        A.free()
+
+
 # Full-size workloads, sampled output rows (the oracle computes them one by one),
 # in the same launch configuration the benchmark times.
 @pytest.mark.parametrize("name,N,s", [("attn13b", 16, 50), ("attn13b", 8, 50), ("ffn13b_up", 64, 50),
