@@ -6,11 +6,13 @@ method's arithmetic: no encoding, no product. Both the oracle tests and the
 GPU tests take their inputs from here.
 """
 from .gen import (  # noqa: F401
+    BLOCKS,
     CONFIGS,
     Instance,
     draw_weights,
     instance_list,
     keep_count,
+    make_block,
     make_instance,
     make_mask,
     make_random,

@@ -257,3 +257,44 @@ def make_small_int(M: int, K: int, N: int, density: float, seed: int, lo: int = 
     mask = (rng.random((M, K)) < density).astype(np.uint8)
     X = _f16_bits(rng.integers(lo, hi + 1, size=(N, K)).astype(np.float64))
     return W, mask, X
+
+
+# Decoder blocks of the synthetic decode-step benchmark: one block's linear
+# layers in execution order, (name, out, in, epilogue), with 13B shapes (hidden
+# 5120, FFN 13824) and 70B-like shapes (hidden 8192, grouped K/V projections of
+# 1024, FFN 28672); the FFN's first layer carries the activation, the output
+# projection and the FFN's last layer a residual add. Weights as the workload
+# set draws them, pruned per row to the given sparsity by magnitude.
+BLOCKS = {
+    "block13b": dict(cfg_id=70, hidden=5120, dist="normal", scale=0.02,
+                     layers=[("q", 5120, 5120, "bias"), ("k", 5120, 5120, "bias"), ("v", 5120, 5120, "bias"),
+                             ("o", 5120, 5120, "bias+residual"), ("up", 13824, 5120, "bias+relu"),
+                             ("down", 5120, 13824, "bias+residual")]),
+    "block70b": dict(cfg_id=80, hidden=8192, dist="student_t4", scale=0.02,
+                     layers=[("q", 8192, 8192, "bias"), ("k", 1024, 8192, "bias"), ("v", 1024, 8192, "bias"),
+                             ("o", 8192, 8192, "bias+residual"), ("up", 28672, 8192, "bias+relu"),
+                             ("down", 8192, 28672, "bias+residual")]),
+}
+
+
+@dataclasses.dataclass
+class BlockLayer:
+    name: str
+    M: int
+    K: int
+    W: np.ndarray       # fp16 bits M x K
+    mask: np.ndarray    # uint8 M x K
+    bias: np.ndarray    # fp16 bits [M]
+    epilogue: str
+
+
+def make_block(name: str, sparsity_pct: int = 50) -> list:
+    cfg = BLOCKS[name]
+    out = []
+    for i, (lname, M, K, epi) in enumerate(cfg["layers"]):
+        cid = cfg["cfg_id"] + i
+        W = draw_weights(cid, M, K, cfg["dist"], cfg["scale"])
+        mask = prune_per_row(_magnitude_bits(W), keep_count(K, sparsity_pct))
+        bias = _f16_bits(seed_for(cid, 3).normal(0.0, cfg["scale"], size=M))
+        out.append(BlockLayer(lname, M, K, W, mask, bias, epi))
+    return out
