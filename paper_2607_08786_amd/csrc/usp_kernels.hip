@@ -53,7 +53,7 @@ constexpr int kWaves = 4;                              // row blocks per workgro
 constexpr int kThreads = kWaves * kLanes;              // 256
 constexpr int kWRegionBytes = kMaxValBytes;            // 8 KB per wavefront (8 KB aligned)
 constexpr int kXRowBytes = kTileK * 2 + 16;            // 528: padded token row of the X tile
-constexpr int kMaxNT = 4;                              // 16-token blocks per pass (N <= 64)
+constexpr int kMaxNT = 8;                              // 16-token blocks per pass (N <= 128)
 constexpr int kWgsPerCu = 3;                           // persistent workgroups per CU
 
 struct SpmmArgs {
@@ -1155,12 +1155,16 @@ static int resident_wgs() {
     return cached;
 }
 
+// Token blocks the four-wavefront kernel is built for: 1-4, and 8 for 5-8.
+static int kernel_nt(int nt) { return nt <= 4 ? nt : kMaxNT; }
+
 static int resident_wgs(int nt, bool xfast) {
-    switch (nt) {
+    switch (kernel_nt(nt)) {
         case 1: return xfast ? resident_wgs<1, true>() : resident_wgs<1, false>();
         case 2: return xfast ? resident_wgs<2, true>() : resident_wgs<2, false>();
         case 3: return xfast ? resident_wgs<3, true>() : resident_wgs<3, false>();
-        default: return xfast ? resident_wgs<4, true>() : resident_wgs<4, false>();
+        case 4: return xfast ? resident_wgs<4, true>() : resident_wgs<4, false>();
+        default: return xfast ? resident_wgs<kMaxNT, true>() : resident_wgs<kMaxNT, false>();
     }
 }
 
@@ -1182,8 +1186,19 @@ static SpmmPlan plan_pass(const usp_matrix *A, int nt) {
     return p;
 }
 
-static int pass_nt(int64_t N, int64_t n0) {
-    const int64_t nb = (N - n0) < 16 * kMaxNT ? (N - n0) : 16 * kMaxNT;
+// Tokens per pass of the four-wavefront kernel (measured on MI355X): 128 for
+// small matrices (at most 8192 tiles; 13B attention at 128 tokens: 39.6 us
+// against 46.3 in two passes of 64), 64 otherwise (the 70B FFN layer at 128
+// tokens: 211 us in one pass, 204 in two: with one workgroup per CU the larger
+// pass is bound by its SIMDs).
+constexpr int64_t kSmallMatrixTiles = 8192;
+static int64_t pass_tokens(const usp_matrix *A) {
+    return A->RB * A->KT <= kSmallMatrixTiles ? 16 * kMaxNT : 64;
+}
+
+static int pass_nt(const usp_matrix *A, int64_t N, int64_t n0) {
+    const int64_t P = pass_tokens(A);
+    const int64_t nb = (N - n0) < P ? (N - n0) : P;
     return (int)((nb + 15) / 16);
 }
 
@@ -1382,7 +1397,7 @@ static bool use_wave_kernel(const usp_matrix *A, const void *X, int64_t ldx, int
     return wave_kind(A, wave_loads(A), N) != kWaveNone;
 }
 
-SpmmPlan plan_spmm(const usp_matrix *A, int64_t N) { return plan_pass(A, pass_nt(N, 0)); }
+SpmmPlan plan_spmm(const usp_matrix *A, int64_t N) { return plan_pass(A, pass_nt(A, N, 0)); }
 
 // Workspace: one uint32 arrival counter per row group at offset 0 (shared by
 // every pass, zero between passes), padded to 256 bytes, then the fp32 partials
@@ -1411,16 +1426,17 @@ static size_t wave_partials_bytes(const usp_matrix *A, int64_t N) {
 
 size_t spmm_workspace_bytes(const usp_matrix *A, int64_t N) {
     // Layout: counters, then the partials of whichever pass runs. Passes run one
-    // after another and reuse the workspace: full passes of 16 * kMaxNT tokens,
-    // then one pass over the remainder; up to 16 tokens may take the wave kernel
-    // (sized here too, whichever needs more).
+    // after another and reuse the workspace: full passes of pass_tokens(A)
+    // tokens, then one pass over the remainder; up to 128 tokens may take a wave
+    // kernel (sized here too, whichever needs more).
     size_t need = N <= kMaxWaveTokens ? wave_partials_bytes(A, N) : 0;
     auto add = [&](int64_t nb) {
         const SpmmPlan p = plan_pass(A, (int)((nb + 15) / 16));
         if (p.split) need = std::max(need, partials_bytes(p, nb));
     };
-    if (N >= 16 * kMaxNT) add(16 * kMaxNT);
-    if (N % (16 * kMaxNT)) add(N % (16 * kMaxNT));
+    const int64_t P = pass_tokens(A);
+    if (N >= P) add(P);
+    if (N % P) add(N % P);
     return need ? counters_bytes(A) + need : 0;
 }
 
@@ -1485,8 +1501,9 @@ int launch_spmm(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_
                 const Epilogue &ep, void *workspace, void *stream) {
     hipStream_t st = reinterpret_cast<hipStream_t>(stream);
     if (use_wave_kernel(A, X, ldx, N)) return launch_wave(A, X, ldx, Y, ldy, N, ep, workspace, st);
-    for (int64_t n0 = 0; n0 < N; n0 += 16 * kMaxNT) {
-        const int nb = (int)((N - n0) < 16 * kMaxNT ? (N - n0) : 16 * kMaxNT);
+    const int64_t P = pass_tokens(A);
+    for (int64_t n0 = 0; n0 < N; n0 += P) {
+        const int nb = (int)((N - n0) < P ? (N - n0) : P);
         const int nt = (nb + 15) / 16;
         const SpmmPlan p = plan_pass(A, nt);
         float *ws = p.split ? reinterpret_cast<float *>(reinterpret_cast<uint8_t *>(workspace) + counters_bytes(A))
@@ -1518,11 +1535,12 @@ int launch_spmm(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_
 #define USP_LAUNCH(NTV)                                                                              \
     if (xfast) hipLaunchKernelGGL((spmm_kernel<NTV, true>), grid, block, 0, st, a, a.off, a.stream); \
     else hipLaunchKernelGGL((spmm_kernel<NTV, false>), grid, block, 0, st, a, a.off, a.stream);
-        switch (nt) {
+        switch (kernel_nt(nt)) {
             case 1: USP_LAUNCH(1) break;
             case 2: USP_LAUNCH(2) break;
             case 3: USP_LAUNCH(3) break;
-            default: USP_LAUNCH(4) break;
+            case 4: USP_LAUNCH(4) break;
+            default: USP_LAUNCH(kMaxNT) break;
         }
 #undef USP_LAUNCH
         const hipError_t e = hipGetLastError();

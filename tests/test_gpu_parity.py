@@ -183,6 +183,25 @@ def test_workspace_contract(torch, usp):
     A.free()
 
 
+# Passes of 128 tokens (small matrices): 200 tokens on 4101 x 1000 run one pass
+# of 128 and one of 72 (last row block ragged, K ends in a partial tile), exact
+# on small integers; 128 tokens on a 13B attention-size random matrix,
+# tolerance.
+def test_wide_token_passes(torch, usp):
+    W, mask, X = wl.make_small_int(4101, 1000, 200, 0.5, seed=81, lo=-1, hi=1)
+    Y = run(torch, usp, W, mask, X)
+    Yref, _ = oracle.masked_gemm(W, mask, X)
+    assert np.array_equal(Y, Yref)
+    W, mask, X = wl.make_random(5120, 5120, 128, 0.5, seed=82)
+    A = usp.SparseMatrix(W, mask)
+    Y = A.spmm(to_dev(torch, X))
+    torch.cuda.synchronize()
+    A.free()
+    rows = np.sort(np.random.default_rng(3).choice(5120, 256, replace=False))
+    got = Y.cpu().numpy().astype(np.float64)[:, rows]
+    assert_close(got, W, mask, X, rows=rows)
+
+
 # One zero-filled workspace shared by handles of different sizes, calls
 # alternating: partials a call leaves behind must never be read as another
 # handle's arrival counters (4101 x 3000 splits its row blocks through the
