@@ -485,24 +485,18 @@ __global__ __launch_bounds__(kThreads, 2) void spmm_kernel(SpmmArgs a, const uin
 }
 
 // ---------------------------------------------------------------------------
-// Barrier-free streaming kernel for up to 16 tokens.
+// Shared parts of the single-pass kernels (up to 128 tokens): the column-chunk,
+// direct-to-LDS and row-block kernels.
 //
-// Every wavefront is its own workgroup and streams its own contiguous range of
-// units with no workgroup barrier: coupling four wavefronts with barriers made
-// each tile wait for the slowest of four loads and halved the achievable HBM
-// rate. A unit is (row set, column tile): R row blocks that share one column
-// tile, so the wavefront loads the tile's MFMA B operands (X, 16 bytes per lane
-// and step) once for R records; X stays resident in L2. One record is in
-// flight: the next record is loaded while the current one is decoded, so only
-// the R accumulators grow with R.
 // All loads go through buffer resources (SGPR base, constant lane offsets,
 // hardware zero-fill out of range). A record is read with L 1 KB loads, L
 // being the smallest count that covers every record of the matrix; the
 // resource ends at the record's own end, so the loads past it fetch nothing.
-// The count per unit is fixed, so the compiler's waits are exact.
-// A row set split over several wavefronts is finished by the last to arrive; a
-// wavefront stores its partial at the end of its segment and counts its arrival
-// at its next unit boundary, where it waits for its loads anyway.
+// The count per record is fixed, so the compiler's waits are exact.
+// A row set whose column tiles are split over several wavefronts (or
+// workgroups) is finished by the last to arrive: each stores its fp32 partial
+// with device-coherent stores, counts its arrival once they are acknowledged,
+// and the last arrival sums the partials in slot order.
 // ---------------------------------------------------------------------------
 
 struct WaveArgs {
@@ -618,26 +612,6 @@ struct WaveRec {
     uint2 msk;
 };
 
-// Loads record (rb, kt); a row block past the matrix (the missing half of the
-// last row set) gets an empty resource, so its mask and values read as zero.
-template <int L>
-__device__ inline void fetch_rec(const WaveArgs &a, const uint32_t *__restrict__ off,
-                                 const uint8_t *__restrict__ stream, int64_t rb, int64_t kt, int lane,
-                                 WaveRec<L> &r) {
-    uint32_t o0 = 0, o1 = 0;
-    if (rb < a.RB) {
-        const int64_t t = rb * a.KT + kt;
-        o0 = off[t];
-        o1 = off[t + 1];
-    }
-    const __amdgpu_buffer_rsrc_t rec = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)(stream + (uint64_t)o0 * 16), (short)0, (int)((o1 - o0) * 16), kBufferRsrcWord3);
-    r.msk = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rec, lane * 8, 0, 0));
-#pragma unroll
-    for (int i = 0; i < L; ++i)
-        r.w[i] = __builtin_amdgcn_raw_buffer_load_b128(rec, kMaskBytes + 1024 * i + lane * 16, 0, 0);
-}
-
 // Loads the record at 16-byte units [o0, o1) into registers.
 template <int L>
 __device__ inline void fetch_rec(const uint8_t *__restrict__ stream, uint32_t o0, uint32_t o1, int lane,
@@ -707,99 +681,108 @@ __device__ inline void decode_record(lds_u32 *slot, const uint8_t *lut, uint2 ms
     }
 }
 
-// R row blocks per unit, L KB of record values per load group.
-template <int R, int L>
-__global__ __launch_bounds__(kLanes) void spmm_wave_kernel(WaveArgs a, const uint32_t *__restrict__ off,
-                                                          const uint8_t *__restrict__ stream) {
-    constexpr int kRegion = 1024 * L + 16;  // staged values + the decode's 12-byte overread
-    __shared__ __attribute__((aligned(16))) uint8_t region[kRegion];
-    __shared__ __attribute__((aligned(16))) uint8_t lut[16 * 8];
-    const int lane = threadIdx.x;
-    const int64_t w = blockIdx.x, G = gridDim.x;
-    const int64_t u0 = w * a.units / G, u1 = (w + 1) * a.units / G;
-    if (u0 >= u1) return;
-    if (lane < 16) reinterpret_cast<uint2 *>(lut)[lane] = nibble_selectors((uint32_t)lane);
-    lds_u32 *const rbase = as_lds(region);
+// ---------------------------------------------------------------------------
+// Column-chunk kernel for small matrices (up to 16 tokens).
+//
+// A workgroup of four wavefronts takes four consecutive row blocks and a chunk
+// of C consecutive column tiles. The chunk's X columns (16 tokens x 256 C
+// halfs) are staged in LDS once, behind the kernel's only barrier. Each
+// wavefront reads the offsets of its C records with one vector load and issues
+// the loads of all C records before decoding the first: on layers this small a
+// wavefront has only a few records, and their round trips, not the HBM rate,
+// set the time, so the wavefront waits about one record's latency instead of
+// one per record (plus one per offset-table entry). The records stay in
+// registers until their turn, then are staged in the wavefront's own LDS region
+// and decoded. The chunks of a row block are summed through the workspace by
+// the last to arrive, in chunk order.
+// ---------------------------------------------------------------------------
 
+constexpr int kChunkTiles = 4;                             // C
+constexpr int kChunkXRow = kChunkTiles * kTileK * 2 + 16;  // padded token row of the chunk's X (bytes)
+
+template <int L>
+__global__ __launch_bounds__(kThreads, 2) void spmm_chunk_kernel(WaveArgs a, const uint32_t *__restrict__ off,
+                                                                 const uint8_t *__restrict__ stream) {
+    constexpr int C = kChunkTiles;
+    constexpr int kRegion = 1024 * L + 16;  // staged values + the decode's 12-byte overread
+    constexpr int kXLoads = 16 * 32 * C / kThreads;  // 16-byte X chunks per thread
+    __shared__ __attribute__((aligned(16))) uint8_t xs[16 * kChunkXRow];
+    __shared__ __attribute__((aligned(16))) uint8_t regions[kWaves * kRegion];
+    __shared__ __attribute__((aligned(16))) uint8_t lut[16 * 8];
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int64_t S = a.maxseg;  // chunks per row block
+    const int64_t rg = blockIdx.x / S, seg = blockIdx.x % S;
+    const int64_t rb = rg * kWaves + wave, kt0 = seg * C;
+    const int nct = (int)(a.KT - kt0 < C ? a.KT - kt0 : C);
+
+    // X of the chunk: token n, 16-byte chunk c of its C * 256 columns; zero for
+    // tokens >= N and columns >= K (read at the resource's end).
     const __amdgpu_buffer_rsrc_t xr =
         __builtin_amdgcn_make_buffer_rsrc((void *)a.X, (short)0, (int)a.x_bytes, kBufferRsrcWord3);
+    v4u32 xv[kXLoads];
+#pragma unroll
+    for (int i = 0; i < kXLoads; ++i) {
+        const int q = tid + kThreads * i, n = q / (32 * C), c = q % (32 * C);
+        const int64_t col = kt0 * kTileK + 8 * c;
+        const int at = (n < a.N && col < a.K) ? (int)((n * a.ldx + col) * 2) : (int)a.x_bytes;
+        xv[i] = __builtin_amdgcn_raw_buffer_load_b128(xr, at, 0, 0);
+    }
+    // Lane j <= nct: offset-table entry j of the wavefront's records.
+    const __amdgpu_buffer_rsrc_t offr =
+        __builtin_amdgcn_make_buffer_rsrc((void *)off, (short)0, (int)((a.RB * a.KT + 1) * 4), kBufferRsrcWord3);
+    const bool real = rb < a.RB && lane <= nct;
+    const uint32_t ov =
+        __builtin_amdgcn_raw_buffer_load_b32(offr, real ? (int)((rb * a.KT + kt0 + lane) * 4) : 0x7FFFFFF0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < kXLoads; ++i) {
+        const int q = tid + kThreads * i, n = q / (32 * C), c = q % (32 * C);
+        *reinterpret_cast<v4u32 *>(xs + n * kChunkXRow + 16 * c) = xv[i];
+    }
+    if (tid < 16) reinterpret_cast<uint2 *>(lut)[tid] = nibble_selectors((uint32_t)tid);
+    // The barrier comes before the records are requested: a wavefront issuing
+    // its record loads can stall for microseconds while the memory system
+    // drains, and its workgroup would wait for that at the barrier.
+    __syncthreads();
+    if (rb >= a.RB) return;
+    WaveRec<L> rec[C];
+#pragma unroll
+    for (int j = 0; j < C; ++j) {
+        const uint32_t o0 = __builtin_amdgcn_readlane(ov, j);
+        const uint32_t o1 = j < nct ? __builtin_amdgcn_readlane(ov, j + 1) : o0;  // past the chunk: empty
+        fetch_rec<L>(stream, o0, o1, lane, rec[j]);
+    }
+
+    uint8_t *const region = regions + wave * kRegion;
+    lds_u32 *const rbase = as_lds(region);
     const int n_lane = lane & 15, g4 = 4 * (lane >> 4);
-    // Lanes of tokens >= N start at the resource's end: every load they issue is
-    // out of range and returns zeros.
-    const int xoff = n_lane < a.N ? (int)(n_lane * a.ldx * 2) + 16 * (lane >> 4) : (int)a.x_bytes;
-
-    floatx4 acc[R];
+    const uint8_t *const xrow = xs + n_lane * kChunkXRow + 2 * 8 * (lane >> 4);
+    floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int r = 0; r < R; ++r) acc[r] = floatx4{0.f, 0.f, 0.f, 0.f};
-    int64_t set = u0 / a.KT, kt = u0 % a.KT;
-    int64_t pend_set = -1, pend_nseg = 0;  // partial stored, arrival not yet counted
-    // One record in flight: record r + 1 (or the next unit's first) is loaded
-    // while record r is decoded.
-    WaveRec<L> cur;
-    fetch_rec<L>(a, off, stream, set * R, kt, lane, cur);
-    for (int64_t u = u0; u < u1; ++u) {
-        int64_t setn = set, ktn = kt + 1;
-        if (ktn == a.KT) {
-            ktn = 0;
-            ++setn;
+    for (int j = 0; j < C; ++j) {
+        if (j < nct) {
+            // In-order LDS: the previous decode's reads of the region are done.
+#pragma unroll
+            for (int i = 0; i < L; ++i) reinterpret_cast<v4u32 *>(region)[lane + kLanes * i] = rec[j].w[i];
+            v4u32 xb[1][kSteps];
+#pragma unroll
+            for (int s = 0; s < kSteps; ++s)
+                xb[0][s] = *reinterpret_cast<const v4u32 *>(xrow + 2 * (j * kTileK + 32 * s));
+            decode_record<1>(rbase, lut, rec[j].msk, xb, reinterpret_cast<floatx4(&)[1]>(acc));
         }
-        const bool more = u + 1 < u1;
-        v4u32 xb[kSteps];
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            // Stage the record (in-order LDS: the previous decode's reads are done).
-#pragma unroll
-            for (int i = 0; i < L; ++i) reinterpret_cast<v4u32 *>(region)[lane + kLanes * i] = cur.w[i];
-            const uint2 msk = cur.msk;
-            if (r == 0) {
-                if (pend_set >= 0) {  // the partial's stores completed with the record's loads
-                    __builtin_amdgcn_s_waitcnt(0);
-                    arrive_row_set<R>(a, pend_set, pend_nseg, lane);
-                    pend_set = -1;
-                }
-                fetch_x(a, xr, xoff, kt, lane, xb);
-            }
-            // Next record (past the range's end: this unit's first again, unused).
-            if (r + 1 < R) fetch_rec<L>(a, off, stream, set * R + r + 1, kt, lane, cur);
-            else fetch_rec<L>(a, off, stream, (more ? setn : set) * R, more ? ktn : kt, lane, cur);
-
-            decode_record<1>(rbase, lut, msk, reinterpret_cast<const v4u32(&)[1][kSteps]>(xb),
-                             reinterpret_cast<floatx4(&)[1]>(acc[r]));
-        }
-
-        if (!more || ktn == 0) {  // end of this wavefront's segment of the row set
-            const int64_t w_first = unit_owner(set * a.KT, a.units, G);
-            const int64_t w_last = unit_owner(set * a.KT + a.KT - 1, a.units, G);
-            if (w_first == w_last) {
-                if (n_lane < a.N) {
-#pragma unroll
-                    for (int r = 0; r < R; ++r) store_rows4(a, n_lane, (set * R + r) * kTileRows + g4, acc[r]);
-                }
-            } else {
-                const int64_t slot_floats = (int64_t)a.N * kTileRows * R;
-                float *slot = a.ws + (set * a.maxseg + (w - w_first)) * slot_floats;
-                const __amdgpu_buffer_rsrc_t part =
-                    __builtin_amdgcn_make_buffer_rsrc(slot, (short)0, (int)(slot_floats * 4), kBufferRsrcWord3);
-                if (n_lane < a.N) {
-#pragma unroll
-                    for (int r = 0; r < R; ++r)
-                        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, acc[r]), part,
-                                                               (n_lane * kTileRows * R + kTileRows * r + g4) * 4, 0,
-                                                               kCachePolicyDevice);
-                }
-                pend_set = set;
-                pend_nseg = w_last - w_first + 1;
-            }
-#pragma unroll
-            for (int r = 0; r < R; ++r) acc[r] = floatx4{0.f, 0.f, 0.f, 0.f};
-        }
-        set = setn;
-        kt = ktn;
     }
-    if (pend_set >= 0) {
-        __builtin_amdgcn_s_waitcnt(0);
-        arrive_row_set<R>(a, pend_set, pend_nseg, lane);
+    if (S == 1) {
+        if (n_lane < a.N) store_rows4(a, n_lane, rb * kTileRows + g4, acc);
+        return;
     }
+    const int64_t slot_floats = (int64_t)a.N * kTileRows;
+    float *slot = a.ws + (rb * S + seg) * slot_floats;
+    const __amdgpu_buffer_rsrc_t part =
+        __builtin_amdgcn_make_buffer_rsrc(slot, (short)0, (int)(slot_floats * 4), kBufferRsrcWord3);
+    if (n_lane < a.N)
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, acc), part, (n_lane * kTileRows + g4) * 4, 0,
+                                               kCachePolicyDevice);
+    __builtin_amdgcn_s_waitcnt(0);  // the partial is acknowledged before the arrival counts
+    arrive_row_set<1>(a, rb, S, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -1203,16 +1186,14 @@ static int pass_nt(const usp_matrix *A, int64_t N, int64_t n0) {
 }
 
 // ---------------------------------------------------------------------------
-// Plans of the single-wavefront kernels (passes of at most 16 tokens).
+// Plans of the single-pass kernels (up to 128 tokens).
 // ---------------------------------------------------------------------------
 
-enum WaveKind { kWaveRegs = 0, kWaveDma4 = 1, kWaveRow = 2, kWaveNone = 3 };
+enum WaveKind { kWaveNone = 0, kWaveDma4 = 1, kWaveRow = 2, kWaveChunk = 3 };
 
-// Row blocks per unit of the register-staged wave kernel, and the smallest
-// number of units a wavefront streams before a split costs it a partial.
-constexpr int kWaveRows = 1;
-constexpr int64_t kMinUnitsPerWave = 4;
 constexpr int kMinWaveLoads = 2;  // record load groups instantiated: 2..8
+// The fewest units a direct-to-LDS wavefront streams before a split costs it a
+// partial.
 constexpr int64_t kMinUnitsPerDmaWave = 2;
 
 // Record load groups (1 KB each) that cover every record of A.
@@ -1285,42 +1266,44 @@ static int row_wpg(const usp_matrix *A, int loads) {
     return 2;
 }
 
-static WaveKernelFn wave_kernel(WaveKind kind, int loads, int nb) {
-#define USP_BY_LOADS(KERNEL, ...)              \
-    switch (loads) {                           \
-        case 2: return KERNEL<2, ##__VA_ARGS__>; \
-        case 3: return KERNEL<3, ##__VA_ARGS__>; \
-        case 4: return KERNEL<4, ##__VA_ARGS__>; \
-        case 5: return KERNEL<5, ##__VA_ARGS__>; \
-        case 6: return KERNEL<6, ##__VA_ARGS__>; \
-        case 7: return KERNEL<7, ##__VA_ARGS__>; \
-        default: return KERNEL<8, ##__VA_ARGS__>; \
+static WaveKernelFn dma_kernel(int loads, int nb) {
+#define USP_BY_LOADS(NB)                            \
+    switch (loads) {                                \
+        case 2: return spmm_dma_kernel<2, NB>;      \
+        case 3: return spmm_dma_kernel<3, NB>;      \
+        case 4: return spmm_dma_kernel<4, NB>;      \
+        case 5: return spmm_dma_kernel<5, NB>;      \
+        case 6: return spmm_dma_kernel<6, NB>;      \
+        case 7: return spmm_dma_kernel<7, NB>;      \
+        default: return spmm_dma_kernel<8, NB>;     \
     }
-    if (kind == kWaveDma4) {
-        if (nb == 1) {
-            USP_BY_LOADS(spmm_dma_kernel, 1)
-        }
-        USP_BY_LOADS(spmm_dma_kernel, 2)
+    if (nb == 1) {
+        USP_BY_LOADS(1)
     }
+    USP_BY_LOADS(2)
 #undef USP_BY_LOADS
+}
+
+static WaveKernelFn chunk_kernel(int loads) {
     switch (loads) {
-        case 2: return spmm_wave_kernel<kWaveRows, 2>;
-        case 3: return spmm_wave_kernel<kWaveRows, 3>;
-        case 4: return spmm_wave_kernel<kWaveRows, 4>;
-        case 5: return spmm_wave_kernel<kWaveRows, 5>;
-        case 6: return spmm_wave_kernel<kWaveRows, 6>;
-        case 7: return spmm_wave_kernel<kWaveRows, 7>;
-        default: return spmm_wave_kernel<kWaveRows, 8>;
+        case 2: return spmm_chunk_kernel<2>;
+        case 3: return spmm_chunk_kernel<3>;
+        case 4: return spmm_chunk_kernel<4>;
+        case 5: return spmm_chunk_kernel<5>;
+        case 6: return spmm_chunk_kernel<6>;
+        case 7: return spmm_chunk_kernel<7>;
+        default: return spmm_chunk_kernel<8>;
     }
 }
 
-// Wavefronts of a wave kernel resident per CU (queried once per variant).
-static int resident_waves(WaveKind kind, int loads, int nb) {
-    static int cached[2][9][kMaxDmaTokenBlocks + 1] = {};
-    int &c = cached[kind][loads][nb];
+// Wavefronts of the direct-to-LDS kernel resident per CU (queried once per
+// variant).
+static int resident_waves(int loads, int nb) {
+    static int cached[9][kMaxDmaTokenBlocks + 1] = {};
+    int &c = cached[loads][nb];
     if (c == 0) {
         int n = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, wave_kernel(kind, loads, nb), kLanes, 0) != hipSuccess ||
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dma_kernel(loads, nb), kLanes, 0) != hipSuccess ||
             n < 1)
             n = 1;
         c = n;
@@ -1339,12 +1322,11 @@ struct WavePlan {
 // kernel once every range gets at least 8 units of 4 row blocks (70B- and
 // 66B-class FFN layers, up to 128 tokens); for small matrices and up to 16
 // tokens, the row-block kernel when there are no more row blocks than CUs (its
-// workgroups then spread evenly) and otherwise the register-staged kernel
-// (13B attention projections: many short single-wavefront ranges balance
-// best); everything else goes to the four-wavefront kernel, which shares X
-// through LDS.
+// workgroups then spread evenly) and otherwise the column-chunk kernel (13B
+// attention projections); everything else goes to the four-wavefront kernel,
+// which shares X through LDS.
 constexpr int64_t kDmaUnitsPerSlot = 8;
-constexpr int64_t kRegsMaxTiles = 8192;
+constexpr int64_t kSmallMaxTiles = 8192;
 static WaveKind wave_kind(const usp_matrix *A, int loads, int64_t N) {
     const int nb = (int)ceil_div(N, 16);
     // Token groups decode every record once per group: measured slower than the
@@ -1352,11 +1334,11 @@ static WaveKind wave_kind(const usp_matrix *A, int loads, int64_t N) {
     if (nb <= kMaxDmaTokenBlocks || (nb > kMinGroupedTokenBlocks && nb <= kMaxDmaTokenBlocks * kMaxDmaTokenGroups)) {
         int nbw, tg;
         dma_tokens(N, nbw, tg);
-        const int64_t slots = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(kWaveDma4, loads, nbw);
+        const int64_t slots = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(loads, nbw);
         if (ceil_div(A->RB, kDmaRows) * A->KT >= kDmaUnitsPerSlot * (slots / tg)) return kWaveDma4;
     }
-    if (nb == 1 && A->RB * A->KT <= kRegsMaxTiles)
-        return A->RB <= (A->num_cus > 0 ? A->num_cus : 256) ? kWaveRow : kWaveRegs;
+    if (nb == 1 && A->RB * A->KT <= kSmallMaxTiles)
+        return A->RB <= (A->num_cus > 0 ? A->num_cus : 256) ? kWaveRow : kWaveChunk;
     return kWaveNone;
 }
 
@@ -1364,17 +1346,32 @@ static WavePlan plan_wave(const usp_matrix *A, int64_t N) {
     WavePlan p;
     p.loads = wave_loads(A);
     p.kind = wave_kind(A, p.loads, N);
-    if (p.kind == kWaveNone || p.kind == kWaveRow) p.kind = kWaveRegs;  // workspace sizing covers every kernel
+    if (p.kind == kWaveChunk) {  // workgroups of 4 row blocks x kChunkTiles column tiles
+        p.rows = 1;
+        p.nb = 1;
+        p.tg = 1;
+        p.sets = A->RB;
+        p.units = A->RB * A->KT;
+        p.maxseg = ceil_div(A->KT, kChunkTiles);
+        p.ranges = ceil_div(A->RB, kWaves) * p.maxseg;
+        p.grid = p.ranges;
+        p.split = p.maxseg > 1;
+        return p;
+    }
     p.nb = 1;
     p.tg = 1;
-    if (p.kind == kWaveDma4) dma_tokens(N, p.nb, p.tg);
-    p.rows = p.kind == kWaveDma4 ? kDmaRows : kWaveRows;
-    const int64_t min_units = p.kind == kWaveDma4 ? kMinUnitsPerDmaWave : kMinUnitsPerWave;
+    if (p.kind != kWaveDma4) {  // the row-block kernel (or none): no partials in the workspace
+        p.rows = 1;
+        p.sets = p.units = p.ranges = p.grid = p.maxseg = 0;
+        p.split = false;
+        return p;
+    }
+    dma_tokens(N, p.nb, p.tg);
+    p.rows = kDmaRows;
     p.sets = ceil_div(A->RB, p.rows);
     p.units = p.sets * A->KT;
-    const int64_t slots =
-        (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(p.kind, p.loads, p.nb) / p.tg;
-    const int64_t want = ceil_div(p.units, min_units);
+    const int64_t slots = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(p.loads, p.nb) / p.tg;
+    const int64_t want = ceil_div(p.units, kMinUnitsPerDmaWave);
     p.ranges = want < slots ? want : slots;
     if (p.tg > 1) p.ranges = std::max<int64_t>(8, p.ranges / 8 * 8);  // whole groups of 8 ranges x tg
     p.grid = p.ranges * p.tg;
@@ -1492,8 +1489,12 @@ static int launch_wave(const usp_matrix *A, const void *X, int64_t ldx, void *Y,
     a.y_vec = ((reinterpret_cast<uintptr_t>(Y) & 7) == 0) && (ldy % 4 == 0);
     a.tg = p.tg;
     set_epilogue(a, ep);
-    hipLaunchKernelGGL(wave_kernel(p.kind, p.loads, p.nb), dim3((unsigned)p.grid), dim3(kLanes), 0, st, a, A->d_off,
-                       reinterpret_cast<const uint8_t *>(A->d_stream));
+    if (p.kind == kWaveChunk)
+        hipLaunchKernelGGL(chunk_kernel(p.loads), dim3((unsigned)p.grid), dim3(kThreads), 0, st, a, A->d_off,
+                           reinterpret_cast<const uint8_t *>(A->d_stream));
+    else
+        hipLaunchKernelGGL(dma_kernel(p.loads, p.nb), dim3((unsigned)p.grid), dim3(kLanes), 0, st, a, A->d_off,
+                           reinterpret_cast<const uint8_t *>(A->d_stream));
     return (int)hipGetLastError();
 }
 

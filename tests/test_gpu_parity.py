@@ -205,7 +205,7 @@ def test_wide_token_passes(torch, usp):
 # One zero-filled workspace shared by handles of different sizes, calls
 # alternating: partials a call leaves behind must never be read as another
 # handle's arrival counters (4101 x 3000 splits its row blocks through the
-# register-staged kernel, 36880 x 8088 through the direct-to-LDS kernel, and
+# column-chunk kernel, 36880 x 8088 through the direct-to-LDS kernel, and
 # 4101 x 1000 at 48 tokens through the four-wavefront kernel). Exact small
 # integers, every output.
 def test_workspace_shared_between_handles(torch, usp):
@@ -315,7 +315,7 @@ def test_mid_tokens_random(torch, usp):
 # Fused epilogue (usp_spmm_ex): Y = act(W X + bias) + residual against the
 # oracle's product through the same epilogue, with the error scale carried
 # through the activation's largest slope. Every kernel: the row-block kernel
-# (1024 x 1024, 16 tokens), the register-staged kernel (4101 x 1000, 16), the
+# (1024 x 1024, 16 tokens), the column-chunk kernel (4101 x 1000, 16), the
 # four-wavefront kernel (48 tokens), the direct-to-LDS kernel (36880 x 8088:
 # 16 tokens, 27 tokens, 100 tokens in token groups).
 EPI_SMALL = [(1024, 1024, 16), (4101, 1000, 16), (4101, 1000, 48)]
@@ -429,17 +429,29 @@ def test_every_instance(torch, usp, name):
         A.free()
 
 
-# More row blocks than CUs but few tiles: the register-staged kernel with its
-# stream-K split across wavefronts (257 row blocks, the last one ragged; K ends
-# in a partial tile), every output checked.
-def test_register_kernel_exact_full(torch, usp):
+# More row blocks than CUs but few tiles: the column-chunk kernel (workgroups
+# of 4 row blocks x 4 column tiles); 257 row blocks (the last one ragged, its
+# row group mostly past M), K ending in a partial tile (one chunk), every
+# output checked.
+def test_chunk_kernel_exact_full(torch, usp):
     W, mask, X = wl.make_small_int(4101, 1000, 16, 0.5, seed=25)
     Y = run(torch, usp, W, mask, X)
     Yref, _ = oracle.masked_gemm(W, mask, X)
     assert np.array_equal(Y, Yref)
 
 
-def test_register_kernel_random_full(torch, usp):
+# Three chunks per row block, summed through the workspace; 13 tokens.
+def test_chunk_kernel_split_random_full(torch, usp):
     W, mask, X = wl.make_random(4101, 3000, 13, 0.45, seed=26)
     Y = run(torch, usp, W, mask, X)
     assert_close(Y, W, mask, X)
+
+
+# Column-chunk kernel with a short last chunk: 6 column tiles (chunks of 4 and
+# 2) and 9 (4, 4 and 1), tokens 16, 7 and 11; exact on small integers.
+@pytest.mark.parametrize("M,K,N", [(4101, 1300, 16), (4101, 1300, 7), (5000, 2200, 11)])
+def test_chunk_kernel_short_last_chunk_exact(torch, usp, M, K, N):
+    W, mask, X = wl.make_small_int(M, K, N, 0.5, seed=M + K + N, lo=-1, hi=1)
+    Y = run(torch, usp, W, mask, X)
+    Yref, _ = oracle.masked_gemm(W, mask, X)
+    assert np.array_equal(Y, Yref)
