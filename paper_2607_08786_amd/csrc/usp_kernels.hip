@@ -1205,17 +1205,18 @@ static int wave_loads(const usp_matrix *A) {
 typedef void (*WaveKernelFn)(WaveArgs, const uint32_t *, const uint8_t *);
 
 // Token blocks of 16 a wavefront of the direct-to-LDS kernel serves (X for all
-// of them stays in registers): 1 or 2; and the most token groups (wavefronts
-// streaming the same units for different tokens).
-constexpr int kMaxDmaTokenBlocks = 2;
+// of them stays in registers): 1 to 4 (3 and 4 leave one wavefront per SIMD);
+// and the most token groups (wavefronts streaming the same units for different
+// tokens).
+constexpr int kMaxDmaTokenBlocks = 4;
 constexpr int kMaxDmaTokenGroups = 4;
-constexpr int kMinGroupedTokenBlocks = 4;  // token groups only above this many blocks
 
-// Token blocks per wavefront and token groups of the direct-to-LDS kernel.
+// Token groups and token blocks per wavefront of the direct-to-LDS kernel: as
+// few groups as hold every block, the blocks spread evenly over them.
 static void dma_tokens(int64_t N, int &nbw, int &tg) {
     const int nb = (int)ceil_div(N, 16);
-    nbw = nb < kMaxDmaTokenBlocks ? nb : kMaxDmaTokenBlocks;
-    tg = (int)ceil_div(nb, nbw);
+    tg = (int)ceil_div(nb, kMaxDmaTokenBlocks);
+    nbw = (int)ceil_div(nb, tg);
 }
 
 // Wavefronts per workgroup of the row-block kernel: 2, 4, 5 or 8.
@@ -1280,7 +1281,13 @@ static WaveKernelFn dma_kernel(int loads, int nb) {
     if (nb == 1) {
         USP_BY_LOADS(1)
     }
-    USP_BY_LOADS(2)
+    if (nb == 2) {
+        USP_BY_LOADS(2)
+    }
+    if (nb == 3) {
+        USP_BY_LOADS(3)
+    }
+    USP_BY_LOADS(4)
 #undef USP_BY_LOADS
 }
 
@@ -1323,22 +1330,28 @@ struct WavePlan {
 // 66B-class FFN layers, up to 128 tokens); for small matrices and up to 16
 // tokens, the row-block kernel when there are no more row blocks than CUs (its
 // workgroups then spread evenly) and otherwise the column-chunk kernel (13B
-// attention projections); everything else goes to the four-wavefront kernel,
-// which shares X through LDS.
+// attention, 13B FFN up) unless a row block would be split into more than 8
+// chunks (13B FFN down: 14 chunks, 29.0 against 27.7 us); everything else goes
+// to the four-wavefront kernel, which shares X through LDS.
 constexpr int64_t kDmaUnitsPerSlot = 8;
 constexpr int64_t kSmallMaxTiles = 8192;
+constexpr int64_t kChunkMaxTiles = 20480;
+constexpr int64_t kChunkMaxSplit = 8;
 static WaveKind wave_kind(const usp_matrix *A, int loads, int64_t N) {
     const int nb = (int)ceil_div(N, 16);
-    // Token groups decode every record once per group: measured slower than the
-    // four-wavefront kernel for 3-4 token blocks, faster for 5-8.
-    if (nb <= kMaxDmaTokenBlocks || (nb > kMinGroupedTokenBlocks && nb <= kMaxDmaTokenBlocks * kMaxDmaTokenGroups)) {
+    // 64 tokens (4 blocks, one wavefront per SIMD) measured slower than the
+    // four-wavefront kernel (107 against 105 us on the 70B FFN); 33-48 tokens
+    // and token groups above 64 faster.
+    if (nb != 4 && nb <= kMaxDmaTokenBlocks * kMaxDmaTokenGroups) {
         int nbw, tg;
         dma_tokens(N, nbw, tg);
         const int64_t slots = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(loads, nbw);
         if (ceil_div(A->RB, kDmaRows) * A->KT >= kDmaUnitsPerSlot * (slots / tg)) return kWaveDma4;
     }
-    if (nb == 1 && A->RB * A->KT <= kSmallMaxTiles)
-        return A->RB <= (A->num_cus > 0 ? A->num_cus : 256) ? kWaveRow : kWaveChunk;
+    if (nb == 1 && A->RB * A->KT <= kSmallMaxTiles && A->RB <= (A->num_cus > 0 ? A->num_cus : 256))
+        return kWaveRow;
+    if (nb == 1 && A->RB * A->KT <= kChunkMaxTiles && ceil_div(A->KT, kChunkTiles) <= kChunkMaxSplit)
+        return kWaveChunk;
     return kWaveNone;
 }
 

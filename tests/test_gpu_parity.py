@@ -277,11 +277,13 @@ def test_dma_kernel_two_token_blocks_ragged(torch, usp):
     assert_close(Y, W, mask, X)
 
 
-# More than 64 tokens: token groups of the direct-to-LDS kernel (wavefronts
-# streaming the same units, 32 tokens each; 33 to 64 tokens take the
-# four-wavefront kernel). Exact on small integers at 64 and 128 tokens,
-# tolerance at 40 and 100 (the last token block partly past N).
-@pytest.mark.parametrize("N", [64, 128])
+# Three and four token blocks per wavefront of the direct-to-LDS kernel, and
+# above 64 tokens its token groups (wavefronts streaming the same units, each
+# for its own blocks; 64 tokens take the four-wavefront kernel). Exact on small
+# integers at 48 (3 blocks), 128 (2 groups of 4) and 176 tokens (groups of 4, 4
+# and 3); tolerance at 40, 100 (2 groups of 4, the last block partly past N)
+# and 250 tokens (4 groups of 4).
+@pytest.mark.parametrize("N", [48, 128, 176])
 def test_dma_kernel_token_groups_exact(torch, usp, N):
     W, mask, X = wl.make_small_int(36880, 8088, N, 0.5, seed=27 + N, lo=-1, hi=1)
     Y = run(torch, usp, W, mask, X)
@@ -289,7 +291,7 @@ def test_dma_kernel_token_groups_exact(torch, usp, N):
     assert np.array_equal(Y, Yref)
 
 
-@pytest.mark.parametrize("N", [40, 100])
+@pytest.mark.parametrize("N", [40, 100, 250])
 def test_dma_kernel_token_groups_ragged(torch, usp, N):
     W, mask, X = wl.make_random(36880, 8088, N, 0.5, seed=28 + N)
     Y = run(torch, usp, W, mask, X)
@@ -445,6 +447,15 @@ def test_chunk_kernel_split_random_full(torch, usp):
     W, mask, X = wl.make_random(4101, 3000, 13, 0.45, seed=26)
     Y = run(torch, usp, W, mask, X)
     assert_close(Y, W, mask, X)
+
+
+# Column-chunk kernel with more workgroups than stay resident at once (13B FFN
+# up shape: 216 row groups x 5 chunks), exact on small integers.
+def test_chunk_kernel_many_workgroups_exact(torch, usp):
+    W, mask, X = wl.make_small_int(13824, 5120, 16, 0.5, seed=91, lo=-1, hi=1)
+    Y = run(torch, usp, W, mask, X)
+    Yref, _ = oracle.masked_gemm(W, mask, X)
+    assert np.array_equal(Y, Yref)
 
 
 # Column-chunk kernel with a short last chunk: 6 column tiles (chunks of 4 and
