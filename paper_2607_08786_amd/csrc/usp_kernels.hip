@@ -645,8 +645,11 @@ __device__ inline void fetch_x(const WaveArgs &a, __amdgpu_buffer_rsrc_t xr, int
 }
 
 // Issue the LDS reads of all 8 steps of a record before expanding any (more
-// registers, shorter chain) instead of one step ahead.
-constexpr bool kDecodeAhead = false;
+// registers, shorter chain) instead of one step ahead: for 3 or more token
+// blocks, where the direct-to-LDS kernel runs one wavefront per SIMD and
+// nothing else hides the LDS latency (1-2% faster there, ~1% slower at one
+// block).
+constexpr int kDecodeAheadMinBlocks = 3;
 
 // Decodes the record in `slot` (mask msk) against the tile's B operands.
 template <int NB>
@@ -655,7 +658,7 @@ __device__ inline void decode_record(lds_u32 *slot, const uint8_t *lut, uint2 ms
     const StepOffsets so = step_offsets(msk);
     const uint32_t tlo0 = (msk.x << 3) & 0x78787878u, thi0 = (msk.x >> 1) & 0x78787878u;
     const uint32_t tlo1 = (msk.y << 3) & 0x78787878u, thi1 = (msk.y >> 1) & 0x78787878u;
-    if (kDecodeAhead) {  // every step's LDS reads first: a short dependency chain per record
+    if (NB >= kDecodeAheadMinBlocks) {  // every step's LDS reads first: a short dependency chain per record
         StepWords all[kSteps];
 #pragma unroll
         for (int s = 0; s < kSteps; ++s) all[s] = read_step(slot, lut, so, s < 4 ? tlo0 : tlo1, s < 4 ? thi0 : thi1, s);
@@ -904,10 +907,13 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
         }
         const bool more = u + 1 < u1;
         const int64_t kp = more ? ktn : kt;  // X of the next unit (past the range's end: this one's, unused)
-        // One token block: the next unit's X is loaded into a second buffer while
-        // this unit is decoded. More: a second buffer would not fit the
-        // registers, so the one buffer is reloaded after the unit's last decode.
-        constexpr bool kXAhead = NB == 1;
+        // The next unit's X is loaded into a second buffer while this unit is
+        // decoded, except at two token blocks: there the second buffer would
+        // cost the second wavefront per SIMD, so the one buffer is reloaded
+        // after the unit's last decode and the next unit waits for it. (At 3 and
+        // 4 blocks the kernel runs one wavefront per SIMD anyway, and the second
+        // buffer fits the 512 registers: 404 and 490, no spills.)
+        constexpr bool kXAhead = NB != 2;
         v4u32 xn[kXAhead ? NB : 1][kSteps];
         uint32_t old = 0;
         // Extents of the unit after next: loaded a whole unit before use.
@@ -1339,10 +1345,7 @@ constexpr int64_t kChunkMaxTiles = 20480;
 constexpr int64_t kChunkMaxSplit = 8;
 static WaveKind wave_kind(const usp_matrix *A, int loads, int64_t N) {
     const int nb = (int)ceil_div(N, 16);
-    // 64 tokens (4 blocks, one wavefront per SIMD) measured slower than the
-    // four-wavefront kernel (107 against 105 us on the 70B FFN); 33-48 tokens
-    // and token groups above 64 faster.
-    if (nb != 4 && nb <= kMaxDmaTokenBlocks * kMaxDmaTokenGroups) {
+    if (nb <= kMaxDmaTokenBlocks * kMaxDmaTokenGroups) {
         int nbw, tg;
         dma_tokens(N, nbw, tg);
         const int64_t slots = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(loads, nbw);

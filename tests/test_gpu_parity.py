@@ -277,13 +277,13 @@ def test_dma_kernel_two_token_blocks_ragged(torch, usp):
     assert_close(Y, W, mask, X)
 
 
-# Three and four token blocks per wavefront of the direct-to-LDS kernel, and
-# above 64 tokens its token groups (wavefronts streaming the same units, each
-# for its own blocks; 64 tokens take the four-wavefront kernel). Exact on small
-# integers at 48 (3 blocks), 128 (2 groups of 4) and 176 tokens (groups of 4, 4
-# and 3); tolerance at 40, 100 (2 groups of 4, the last block partly past N)
-# and 250 tokens (4 groups of 4).
-@pytest.mark.parametrize("N", [48, 128, 176])
+# Three and four token blocks per wavefront of the direct-to-LDS kernel (X
+# double-buffered, all 8 steps' LDS reads issued first), and above 64 tokens
+# its token groups (wavefronts streaming the same units, each for its own
+# blocks). Exact on small integers at 48 (3 blocks), 64 (4), 128 (2 groups of
+# 4) and 176 tokens (groups of 4, 4 and 3); tolerance at 40, 100 (2 groups of
+# 4, the last block partly past N) and 250 tokens (4 groups of 4).
+@pytest.mark.parametrize("N", [48, 64, 128, 176])
 def test_dma_kernel_token_groups_exact(torch, usp, N):
     W, mask, X = wl.make_small_int(36880, 8088, N, 0.5, seed=27 + N, lo=-1, hi=1)
     Y = run(torch, usp, W, mask, X)
