@@ -449,6 +449,17 @@ def test_chunk_kernel_split_random_full(torch, usp):
     assert_close(Y, W, mask, X)
 
 
+# 17 to 32 tokens on small matrices with more row blocks than CUs (the
+# four-wavefront kernel): K of 2, 9 and 6 column tiles, ragged tokens; exact on
+# small integers.
+@pytest.mark.parametrize("M,K,N", [(4101, 512, 32), (5000, 2200, 20), (4101, 1300, 27)])
+def test_two_token_blocks_small_exact(torch, usp, M, K, N):
+    W, mask, X = wl.make_small_int(M, K, N, 0.5, seed=M + 3 * K + N, lo=-1, hi=1)
+    Y = run(torch, usp, W, mask, X)
+    Yref, _ = oracle.masked_gemm(W, mask, X)
+    assert np.array_equal(Y, Yref)
+
+
 # Column-chunk kernel with more workgroups than stay resident at once (13B FFN
 # up shape: 216 row groups x 5 chunks), exact on small integers.
 def test_chunk_kernel_many_workgroups_exact(torch, usp):
