@@ -1340,7 +1340,9 @@ struct WavePlan {
 // chunks (13B FFN down: 14 chunks, 29.0 against 27.7 us); everything else goes
 // to the four-wavefront kernel, which shares X through LDS.
 constexpr int64_t kDmaUnitsPerSlot = 8;
+constexpr int64_t kMaxDmaWideSplit = 4;
 constexpr int64_t kSmallMaxTiles = 8192;
+constexpr int64_t kRowMaxTiles = 16;  // column tiles per row block
 constexpr int64_t kChunkMaxTiles = 20480;
 constexpr int64_t kChunkMaxSplit = 8;
 static WaveKind wave_kind(const usp_matrix *A, int loads, int64_t N) {
@@ -1349,9 +1351,22 @@ static WaveKind wave_kind(const usp_matrix *A, int loads, int64_t N) {
         int nbw, tg;
         dma_tokens(N, nbw, tg);
         const int64_t slots = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(loads, nbw);
-        if (ceil_div(A->RB, kDmaRows) * A->KT >= kDmaUnitsPerSlot * (slots / tg)) return kWaveDma4;
+        const int64_t sets = ceil_div(A->RB, kDmaRows);
+        // At 3-4 blocks (one wavefront per SIMD, 16 KB partials per row set at
+        // 64 tokens) a row set split over more than 4 wavefronts costs more than
+        // the four-wavefront kernel: the 70B FFN down projection (8192 x 28672,
+        // 128 row sets over 1024 wavefronts) takes 107.9 us against 101.3 at 64
+        // tokens, while the up projection (448 row sets) gains.
+        const bool split_ok = nbw < 3 || sets * kMaxDmaWideSplit >= slots / tg;
+        if (split_ok && sets * A->KT >= kDmaUnitsPerSlot * (slots / tg)) return kWaveDma4;
     }
-    if (nb == 1 && A->RB * A->KT <= kSmallMaxTiles && A->RB <= (A->num_cus > 0 ? A->num_cus : 256))
+    // The row-block kernel for few long row blocks only while each has few
+    // column tiles or the tokens are few: one GPU's share of the 70B FFN
+    // (224 row blocks x 32 tiles) takes 16.8 us on it at 16 tokens against 14.8
+    // on the column-chunk kernel, but 13.6 against 14.5 at 8 tokens; the tiny
+    // layer (4 tiles) 4.5 against 6.6.
+    if (nb == 1 && A->RB * A->KT <= kSmallMaxTiles && A->RB <= (A->num_cus > 0 ? A->num_cus : 256) &&
+        (A->KT <= kRowMaxTiles || N <= 8))
         return kWaveRow;
     if (nb == 1 && A->RB * A->KT <= kChunkMaxTiles && ceil_div(A->KT, kChunkTiles) <= kChunkMaxSplit)
         return kWaveChunk;

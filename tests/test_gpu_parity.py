@@ -460,6 +460,16 @@ def test_two_token_blocks_small_exact(torch, usp, M, K, N):
     assert np.array_equal(Y, Yref)
 
 
+# One GPU's share of the 70B FFN under 8-way row sharding (3584 x 8192: fewer
+# row blocks than CUs, so the K dimension is split), every output against the
+# oracle's tolerance.
+@pytest.mark.parametrize("N", [16, 64])
+def test_sharded_layer_full(torch, usp, N):
+    inst = wl.make_instance("ffn70b_shard8", N)
+    Y = run(torch, usp, inst.W, inst.mask, inst.X)
+    assert_close(Y, inst.W, inst.mask, inst.X)
+
+
 # Column-chunk kernel with more workgroups than stay resident at once (13B FFN
 # up shape: 216 row groups x 5 chunks), exact on small integers.
 def test_chunk_kernel_many_workgroups_exact(torch, usp):

@@ -74,3 +74,16 @@ def test_colscale_makes_column_density_nonuniform():
 
 def test_instance_list_size():
     assert len(wl.instance_list()) == 38
+
+
+# A shard is the first M/8 rows of its layer: whole seed chunks reproduce the
+# layer's rows exactly, and per-row pruning keeps each row's mask its own.
+def test_shard_rows_match_layer():
+    sh = wl.make_instance("ffn70b_shard8", 1)
+    assert (sh.M, sh.K, sh.sparsity_pct) == (3584, 8192, 50)
+    full_rows = wl.draw_weights(5, 2048, 8192, "student_t4", 0.02)
+    assert np.array_equal(full_rows, sh.W[:2048])
+    assert np.array_equal(wl.make_x(5, 8192, 1), sh.X)
+    kept = sh.mask.sum(axis=1)
+    assert np.all(kept == wl.keep_count(8192, 50))
+    assert len(wl.instance_list()) == 38

@@ -8,10 +8,12 @@ GPU tests take their inputs from here.
 from .gen import (  # noqa: F401
     BLOCKS,
     CONFIGS,
+    SHARDS,
     Instance,
     draw_weights,
     instance_list,
     keep_count,
+    layer_config,
     make_block,
     make_instance,
     make_mask,

@@ -198,6 +198,23 @@ CONFIGS = {
 }
 
 
+# One GPU's share of a layer under row sharding (not part of the workload set
+# above): the first M rows drawn with the layer's generator and seeds. Per-row
+# pruning makes each row's mask independent of the others; rows of a partly
+# drawn seed chunk are drawn from the same distribution as the full layer's.
+SHARDS = {
+    "ffn70b_shard8": dict(base="ffn70b", M=28672 // 8, sparsity=(50,)),  # 70B FFN over 8 GPUs: 3584 x 8192
+}
+
+
+def layer_config(name: str) -> dict:
+    """The shape and generator settings of a workload or of a shard."""
+    if name in SHARDS:
+        sh = SHARDS[name]
+        return dict(CONFIGS[sh["base"]], M=sh["M"], sparsity=sh["sparsity"])
+    return CONFIGS[name]
+
+
 def make_mask(cfg: dict, W: np.ndarray, sparsity_pct: int) -> np.ndarray:
     M, K = W.shape
     kind = cfg["prune"]
@@ -221,7 +238,7 @@ def make_mask(cfg: dict, W: np.ndarray, sparsity_pct: int) -> np.ndarray:
 
 
 def make_instance(name: str, N: int, sparsity_pct: int | None = None) -> Instance:
-    cfg = CONFIGS[name]
+    cfg = layer_config(name)
     s = cfg["sparsity"][0] if sparsity_pct is None else sparsity_pct
     W = draw_weights(cfg["cfg_id"], cfg["M"], cfg["K"], cfg["dist"], cfg["scale"])
     mask = make_mask(cfg, W, s)
