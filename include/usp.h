@@ -87,7 +87,10 @@ size_t usp_workspace_size(const usp_matrix *A, int64_t N);
  * Accumulation is fp32 in a fixed order: results are bitwise reproducible run
  * to run. The output is rounded to fp16 with round-to-nearest-even.
  * Inputs with X not 16-byte aligned or ldx not a multiple of 8 take a slower
- * element-wise path. No allocation and no synchronisation happens inside.
+ * element-wise path. No allocation and no synchronisation happens inside, and
+ * the call only enqueues kernels on `stream` (no memory-set or copy operations),
+ * so it may be captured into a HIP graph and the graph replayed; each replay
+ * leaves the workspace ready for the next, as each call does.
  */
 usp_status usp_spmm(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy,
                     int64_t N, void *workspace, size_t ws_bytes, void *stream);

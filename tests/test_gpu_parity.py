@@ -487,3 +487,43 @@ def test_chunk_kernel_short_last_chunk_exact(torch, usp, M, K, N):
     Y = run(torch, usp, W, mask, X)
     Yref, _ = oracle.masked_gemm(W, mask, X)
     assert np.array_equal(Y, Yref)
+
+
+# Capture in a HIP graph (as the benchmark does): two products per graph with
+# their own workspace, replayed five times with eager work (an X update and an
+# eager product) in between; every replay must equal the eager result bit for
+# bit. The graph holds only the library's kernels (no memset node), and split
+# products must leave their arrival counters at zero for the next replay. Every
+# kernel: row-block (1024 x 1024, 16), column-chunk (5120 x 5120, 16, 5 chunks
+# per row block), direct-to-LDS (36880 x 8088 at 16 and 100 tokens), and
+# four-wavefront (4101 x 1000, 48).
+@pytest.mark.parametrize("M,K,N", [(1024, 1024, 16), (5120, 5120, 16), (36880, 8088, 16), (36880, 8088, 100),
+                                   (4101, 1000, 48)])
+def test_graph_capture_replays(torch, usp, M, K, N):
+    W, mask, X = wl.make_random(M, K, N, 0.5, seed=M + N)
+    A = usp.SparseMatrix(W, mask)
+    Xd = to_dev(torch, X)
+    ws = A.make_workspace(N)
+    Yg = torch.empty((N, M), dtype=torch.float16, device="cuda")
+    Ye = torch.empty_like(Yg)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):  # warm-up outside the capture
+        A.spmm(Xd, Yg, workspace=ws)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        A.spmm(Xd, Yg, workspace=ws)
+        A.spmm(Xd, Yg, workspace=ws)
+    ws_eager = A.make_workspace(N)
+    for rep in range(5):
+        Xd.mul_(-1.0 if rep % 2 else 1.0)  # eager work between replays (exact: sign flips)
+        g.replay()
+        A.spmm(Xd, Ye, workspace=ws_eager)
+        torch.cuda.synchronize()
+        assert torch.equal(Yg, Ye), (M, K, N, rep)
+    if ws is not None:  # arrival counters (4 bytes per row block, rounded to sets of 4) back at zero
+        RB = (M + 15) // 16
+        assert int(ws[: 16 * ((RB + 3) // 4)].count_nonzero().item()) == 0
+    A.free()
