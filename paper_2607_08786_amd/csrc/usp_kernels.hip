@@ -1,36 +1,36 @@
 // usp_kernels.hip -- gfx950 kernels of the sparse product and their launchers.
 //
-// Work decomposition. A workgroup is 4 wavefronts; wavefront w owns row block
-// 4 rg + w of a row group rg (64 rows), and the 4 wavefronts walk the same
-// 256-column tiles in lockstep. The work is the sequence of units
-// (row group, column tile) in row-group-major order; the grid is persistent
-// (a fixed number of workgroups per CU) and workgroup w takes the contiguous
-// units [w U / G, (w+1) U / G), so every workgroup streams the same number of
-// tiles. A row group whose columns are split over several workgroups is
-// finished by whichever of them arrives last (see below).
-// Per tile:
-//   * the workgroup stages the X tile (N tokens x 256 columns, fp16) into LDS
-//     once; all 4 wavefronts read their MFMA B operands from it;
-//   * each wavefront stages its own compressed tile record into its LDS region;
-//     the next two tiles' records and X tiles are already being fetched into
-//     registers while the current one is decoded;
-//   * per 32-column step, a wavefront prefix sum of the lanes' kept counts gives
-//     each lane the start of its packed values (the decode is a prefix sum over
-//     the metadata, as the paper's PDD decode in Section 4.3 is); three packed
-//     DPP scans per tile cover all 8 steps;
+// Four kernels share one decode; the planner (wave_kind, plan_wave, plan_pass)
+// picks one by shape and token count:
+//   * spmm_dma_kernel (large layers, up to 256 tokens): one wavefront per
+//     workgroup streams a contiguous range of units (4 row blocks x 1 column
+//     tile), records moved straight into a ring of LDS slots, X in registers;
+//     more than 4 blocks of 16 tokens are split into token groups;
+//   * spmm_chunk_kernel (small layers, up to 16 tokens): 4 row blocks x a chunk
+//     of 4 column tiles per workgroup, every record requested at once;
+//   * spmm_row_kernel (few row blocks, up to 16 tokens): one row block per
+//     workgroup, its column tiles split over the wavefronts and summed in LDS;
+//   * spmm_kernel (everything else, any token count in passes): a workgroup of
+//     4 wavefronts walks the column tiles of one row group (64 rows) at a time,
+//     the X tile staged in LDS once per tile for all 4, one tile in flight.
+// Per record, whatever the kernel:
+//   * a wavefront prefix sum of the lanes' kept counts gives each lane the start
+//     of its packed values at every 32-column step (the decode is a prefix sum
+//     over the metadata, as the paper's PDD decode in Section 4.3 is); three
+//     packed DPP scans cover all 8 steps;
 //   * each lane expands its 8 positions of the step into the 16 x 32 fp16 A
 //     operand: two nibble expansions, each a funnel shift (v_alignbyte) of three
 //     LDS dwords plus two byte permutes (v_perm) driven by a 16-entry selector
 //     table;
 //   * v_mfma_f32_16x16x32_f16 accumulates in fp32 (the dense-contraction part,
 //     Section 4.3).
-// Epilogue of a row group: fp32 -> fp16 with round to nearest even. When the
-// row group's columns were split, each contributing workgroup writes its fp32
-// partial sums with device-coherent stores and bumps the row group's counter;
-// the last to arrive reads every partial with device-coherent loads, sums them
-// in a fixed order (bitwise reproducible, no floating-point atomics), stores Y
-// and resets the counter to zero for the next call. No workgroup waits on
-// another.
+// Epilogue: fp32 -> optional bias, activation and residual -> fp16 with round
+// to nearest even. A row block (or row group) whose columns were split over
+// several wavefronts or workgroups is finished by whichever arrives last: each
+// writes its fp32 partial sums with device-coherent stores and bumps a counter;
+// the last reads every partial with device-coherent loads, sums them in a fixed
+// order (bitwise reproducible, no floating-point atomics), stores Y and resets
+// the counter to zero for the next call. No workgroup waits on another.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -789,13 +789,14 @@ __global__ __launch_bounds__(kThreads, 2) void spmm_chunk_kernel(WaveArgs a, con
 }
 
 // ---------------------------------------------------------------------------
-// Direct-to-LDS variant of the wave kernel (4 row blocks per unit).
+// Direct-to-LDS kernel (4 row blocks per unit).
 //
 // Records are loaded by buffer-to-LDS transfers into a ring of four LDS slots,
 // one per row block of the unit, so three records are in flight while one is
 // decoded and no VGPRs hold them. Each slot is its own LDS array: the compiler
-// waits for exactly the transfers into the slot a decode reads. The unit's X
-// operands are loaded into registers one unit ahead.
+// waits for exactly the transfers into the slot a decode reads. The next unit's
+// X operands are loaded into a second register buffer during the unit (except
+// at 2 token blocks, see below).
 // More tokens than one wavefront's registers hold X for are split into token
 // groups: tg wavefronts stream the same units, each for its own NB blocks of 16
 // tokens, and decode every record. Workgroups are dispatched to the eight XCDs
@@ -1413,7 +1414,7 @@ static WavePlan plan_wave(const usp_matrix *A, int64_t N) {
     return p;
 }
 
-// The wave kernels serve single passes (up to 128 tokens) with X 16-byte
+// The single-pass kernels serve up to 256 tokens with X 16-byte
 // aligned, ldx and K multiples of 8, and X's extent and the offset table
 // addressable by 32-bit offsets.
 constexpr int64_t kMaxWaveTokens = 16 * kMaxDmaTokenBlocks * kMaxDmaTokenGroups;
