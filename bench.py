@@ -118,6 +118,41 @@ def stream_copy_gbps(torch, nbytes=1 << 30, reps=10):
     return gbps
 
 
+def same_size_read_us(torch, nbytes, reps=200, waves=4096):
+    """Per-call time of a plain streaming read of nbytes (usp_probe_read: 1 KB
+    loads per wavefront, 8 in flight, nothing written), back to back and
+    rotating over >= 1 GiB of buffers so the bytes come from HBM: what a kernel
+    that only reads the same bytes takes at this size, launch and ramp
+    included."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2607_08786_amd",
+                                   "libusp_probe.so"))
+    lib.usp_probe_read.restype = ctypes.c_int
+    lib.usp_probe_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    copies = max(2, -(-(1 << 30) // nbytes))
+    bufs = [torch.ones(nbytes, dtype=torch.uint8, device="cuda") for _ in range(copies)]
+    sink = torch.zeros(waves, dtype=torch.int32, device="cuda")
+    st = torch.cuda.current_stream().cuda_stream
+
+    def call(i):
+        rc = lib.usp_probe_read(bufs[i % copies].data_ptr(), nbytes, waves, sink.data_ptr(), st)
+        if rc != 0:
+            raise RuntimeError(f"usp_probe_read failed: {rc}")
+
+    for i in range(copies):
+        call(i)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(reps):
+        call(i)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    del bufs
+    return us
+
+
 def cpu_baseline(inst, seconds):
     import oracle
     lib = oracle.load()
@@ -379,6 +414,9 @@ def main():
         peak = stream_copy_gbps(torch)
         out["stream_copy_GBps"] = peak
         out["frac_of_stream_copy"] = achieved / peak
+        rd = same_size_read_us(torch, wbytes)
+        out["same_size_read"] = {"us": rd, "GBps": wbytes / rd / 1e3, "bytes": wbytes,
+                                 "frac_of_same_size_read": rd / (ms * 1e3)}  # read time / product time
     if args.calibrate_copy:
         src = torch.empty(256 * 2**20, dtype=torch.uint8, device="cuda").fill_(1)
         dst = torch.empty_like(src)

@@ -28,7 +28,26 @@ def build(verbose: bool = False) -> str:
         sys.stderr.write(res.stdout + res.stderr)
         raise RuntimeError("hipcc failed building libusp.so")
     os.replace(tmp, LIB)
+    build_probe(verbose)
     return LIB
+
+
+PROBE_LIB = os.path.join(HERE, "libusp_probe.so")
+
+
+def build_probe(verbose: bool = False) -> str:
+    """libusp_probe.so: the plain streaming read the benchmark reports as a reference."""
+    tmp = PROBE_LIB + ".tmp"
+    cmd = [HIPCC, *DEVICE_FLAGS, "-O3", "-std=c++17", "-fPIC", "-shared", "-Wall",
+           os.path.join(CSRC, "usp_probe.hip"), "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        sys.stderr.write(res.stdout + res.stderr)
+        raise RuntimeError("hipcc failed building libusp_probe.so")
+    os.replace(tmp, PROBE_LIB)
+    return PROBE_LIB
 
 
 if __name__ == "__main__":

@@ -77,3 +77,14 @@ def test_sparse_linear_op_is_registered():
         x = torch.empty(7, 64, dtype=torch.float16)
         y = torch.ops.usp.sparse_linear(x, 0, 33, None, None, 1, None)
     assert tuple(y.shape) == (7, 33) and y.dtype == torch.float16
+
+
+# The benchmark's streaming-read reference library builds and exports its entry
+# point (no GPU call here).
+def test_probe_library_exports_read():
+    import ctypes
+    import os
+    path = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "paper_2607_08786_amd",
+                        "libusp_probe.so")
+    lib = ctypes.CDLL(path)
+    assert hasattr(lib, "usp_probe_read")
