@@ -460,6 +460,20 @@ def test_two_token_blocks_small_exact(torch, usp, M, K, N):
     assert np.array_equal(Y, Yref)
 
 
+# More than 256 tokens on a large matrix: passes of 64 tokens of the
+# four-wavefront kernel reusing one workspace, the row groups split across
+# workgroups in every pass (300 tokens: 4 passes of 64 and one of 44); exact on
+# small integers for 512 sampled rows, and the last row group (ragged, 1 real
+# row block).
+def test_many_passes_large_matrix_exact(torch, usp):
+    W, mask, X = wl.make_small_int(36880, 8088, 300, 0.5, seed=93, lo=-1, hi=1)
+    Y = run(torch, usp, W, mask, X)
+    rng = np.random.default_rng(5)
+    rows = np.unique(np.concatenate([rng.choice(36864, 512, replace=False), np.arange(36864, 36880)]))
+    Yref, _ = oracle.masked_gemm(W, mask, X, rows=rows)
+    assert np.array_equal(Y[:, rows], Yref)
+
+
 # One GPU's share of the 70B FFN under 8-way row sharding (3584 x 8192: fewer
 # row blocks than CUs, so the K dimension is split), every output against the
 # oracle's tolerance.
