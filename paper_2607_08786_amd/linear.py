@@ -56,7 +56,7 @@ class SparseLinear(torch.nn.Module):
         self.activation = activation
         self.register_buffer(
             "bias", None if bias is None else bias.detach().to(device=f"cuda:{dev}", dtype=torch.float16).contiguous())
-        self._ws: dict = {}
+        self._ws: Optional[torch.Tensor] = None  # one workspace for every N, grown when a call needs more
 
     @classmethod
     def from_linear(cls, linear: torch.nn.Linear, mask, activation: str = "none") -> "SparseLinear":
@@ -64,9 +64,16 @@ class SparseLinear(torch.nn.Module):
         return cls(linear.weight, mask, linear.bias, activation, dev)
 
     def workspace(self, N: int) -> Optional[torch.Tensor]:
-        if N not in self._ws:
-            self._ws[N] = self.matrix.make_workspace(N)
-        return self._ws[N]
+        """A zero-filled workspace of at least usp_workspace_size(N) bytes. Every
+        completed call leaves a workspace ready for the next call with any N, so
+        one buffer serves all token counts; it is replaced (zero-filled again) only
+        when a token count needs more bytes than it has."""
+        need = self.matrix.workspace_size(N)
+        if need == 0:
+            return self._ws
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = self.matrix.make_workspace(N)
+        return self._ws
 
     def forward(self, x: torch.Tensor, residual: Optional[torch.Tensor] = None) -> torch.Tensor:
         lead = x.shape[:-1]

@@ -396,6 +396,15 @@ def test_sparse_linear_module(torch, usp):
     yref, scale = oracle.linear_epilogue(Yref, Aref, 1, bias=b64, residual=r64)
     out = oracle.check_tolerance(y.reshape(16, 4101).cpu().numpy().astype(np.float64), yref, scale)
     assert out["ok"], out
+    # One workspace for every token count: 48 tokens (split row groups) and then
+    # 16 and 48 again through the same module equal a fresh module's results.
+    x48 = torch.randn(48, 1000, device="cuda", dtype=torch.float16)
+    ya = mod(x48)
+    yb = mod(x)
+    yc = mod(x48)
+    fresh = SparseLinear.from_linear(lin, mask, activation="relu")
+    torch.cuda.synchronize()
+    assert torch.equal(ya, yc) and torch.equal(ya, fresh(x48)) and torch.equal(yb, fresh(x))
 
 
 # Every instance of the workload set (6 layers x sparsities x token counts, 38
