@@ -126,6 +126,16 @@ usp_status usp_spmm_ex(const usp_matrix *A, const void *X, int64_t ldx, void *Y,
                        void *workspace, size_t ws_bytes, void *stream);
 
 /*
+ * usp_plan -- which kernel usp_spmm runs for this handle and N when X is 16-byte
+ * aligned with ldx = K, as a short text ("row W=8", "chunk S=5 grid=400",
+ * "dma nb=4 tg=1 grid=1024", "fourwave passes=1 nt=2 grid=768"), written to
+ * buf (at most len bytes with the terminating NUL, truncated if longer). For
+ * tests and tuning; enqueues nothing. USP_ERR_INVALID_ARG for a NULL handle,
+ * N < 1, or no buffer.
+ */
+usp_status usp_plan(const usp_matrix *A, int64_t N, char *buf, size_t len);
+
+/*
  * usp_densify -- writes W with the mask applied (pruned entries as +0) into a
  * dense row-major M x K fp16 device buffer Wd with row stride ldw >= K, by the
  * same on-chip decode the product uses. Asynchronous on `stream`. For checks.

@@ -104,6 +104,18 @@ size_t usp_workspace_size(const usp_matrix *A, int64_t N) {
     return usp::spmm_workspace_bytes(A, N);
 }
 
+usp_status usp_plan(const usp_matrix *A, int64_t N, char *buf, size_t len) {
+    if (!alive(A)) return usp::fail(USP_ERR_INVALID_ARG, "usp_plan: invalid or freed handle");
+    if (N < 1 || !buf || len == 0) return usp::fail(USP_ERR_INVALID_ARG, "usp_plan: need N >= 1 and a buffer");
+    DeviceGuard g(A->device);
+    if (!g.ok) return usp::fail(USP_ERR_HIP, "usp_plan: cannot select device");
+    const std::string d = usp::describe_plan(A, N);
+    const size_t n = d.size() < len - 1 ? d.size() : len - 1;
+    std::memcpy(buf, d.data(), n);
+    buf[n] = '\0';
+    return USP_OK;
+}
+
 static usp_status spmm_common(const char *fn, const usp_matrix *A, const void *X, int64_t ldx, void *Y,
                               int64_t ldy, int64_t N, const usp::Epilogue &ep, void *workspace, size_t ws_bytes,
                               void *stream) {

@@ -53,6 +53,8 @@ struct SpmmPlan {
 };
 SpmmPlan plan_spmm(const usp_matrix *A, int64_t N);
 size_t spmm_workspace_bytes(const usp_matrix *A, int64_t N);
+// The kernel usp_spmm runs for A and N (X 16-byte aligned, ldx = K), as text.
+std::string describe_plan(const usp_matrix *A, int64_t N);
 // Fused output epilogue: Y = act(W X + bias) + residual (all optional).
 struct Epilogue {
     const uint16_t *bias = nullptr;  // fp16 [M]

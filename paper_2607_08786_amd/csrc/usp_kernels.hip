@@ -34,6 +34,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdio>
+#include <string>
 
 #include "usp_internal.h"
 
@@ -1427,6 +1429,30 @@ static bool use_wave_kernel(const usp_matrix *A, const void *X, int64_t ldx, int
 }
 
 SpmmPlan plan_spmm(const usp_matrix *A, int64_t N) { return plan_pass(A, pass_nt(A, N, 0)); }
+
+std::string describe_plan(const usp_matrix *A, int64_t N) {
+    char buf[128];
+    // As launch_spmm decides for X 16-byte aligned with ldx = K.
+    if (use_wave_kernel(A, reinterpret_cast<const void *>(uintptr_t{256}), A->K, N)) {
+        const int loads = wave_loads(A);
+        const WaveKind kind = wave_kind(A, loads, N);
+        if (kind == kWaveRow) {
+            snprintf(buf, sizeof buf, "row W=%d", row_wpg(A, loads));
+        } else {
+            const WavePlan p = plan_wave(A, N);
+            if (kind == kWaveChunk)
+                snprintf(buf, sizeof buf, "chunk S=%lld grid=%lld", (long long)p.maxseg, (long long)p.grid);
+            else
+                snprintf(buf, sizeof buf, "dma nb=%d tg=%d grid=%lld", p.nb, p.tg, (long long)p.grid);
+        }
+        return buf;
+    }
+    const int64_t P = pass_tokens(A);
+    const SpmmPlan p = plan_pass(A, pass_nt(A, N, 0));
+    snprintf(buf, sizeof buf, "fourwave passes=%lld nt=%d grid=%lld", (long long)ceil_div(N, P), pass_nt(A, N, 0),
+             (long long)p.grid);
+    return buf;
+}
 
 // Workspace: one uint32 arrival counter per row group at offset 0 (shared by
 // every pass, zero between passes), padded to 256 bytes, then the fp32 partials

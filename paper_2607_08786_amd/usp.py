@@ -20,8 +20,8 @@ USP_OK = 0
 _STATUS = {0: "USP_OK", 1: "USP_ERR_INVALID_ARG", 2: "USP_ERR_UNSUPPORTED", 3: "USP_ERR_OOM",
            4: "USP_ERR_HIP", 5: "USP_ERR_INTERNAL"}
 
-EXPORTED = ("usp_encode", "usp_workspace_size", "usp_spmm", "usp_spmm_ex", "usp_densify", "usp_decode",
-            "usp_info", "usp_free", "usp_last_error")
+EXPORTED = ("usp_encode", "usp_workspace_size", "usp_spmm", "usp_spmm_ex", "usp_plan", "usp_densify",
+            "usp_decode", "usp_info", "usp_free", "usp_last_error")
 
 # usp_activation
 ACTIVATIONS = {"none": 0, "relu": 1, "gelu_tanh": 2, "silu": 3}
@@ -62,6 +62,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.usp_spmm.restype = st
     lib.usp_spmm_ex.argtypes = [p, p, i64, p, i64, i64, p, p, i64, ctypes.c_int, p, sz, p]
     lib.usp_spmm_ex.restype = st
+    lib.usp_plan.argtypes = [p, i64, ctypes.c_char_p, sz]
+    lib.usp_plan.restype = st
     lib.usp_densify.argtypes = [p, p, i64, p]
     lib.usp_densify.restype = st
     lib.usp_decode.argtypes = [p, p, p]
@@ -114,6 +116,13 @@ def usp_encode(W: np.ndarray, mask: np.ndarray, device: int = 0) -> int:
 
 def usp_workspace_size(handle: int, N: int) -> int:
     return int(load_library().usp_workspace_size(handle, N))
+
+
+def usp_plan(handle: int, N: int) -> str:
+    """The kernel usp_spmm runs for this handle and N (X aligned, ldx = K), as text."""
+    buf = ctypes.create_string_buffer(128)
+    _check(load_library().usp_plan(handle, N, buf, len(buf)))
+    return buf.value.decode()
 
 
 def usp_spmm(handle: int, X: torch.Tensor, Y: torch.Tensor, workspace: torch.Tensor | None = None,
@@ -201,6 +210,9 @@ class SparseMatrix:
 
     def workspace_size(self, N: int) -> int:
         return usp_workspace_size(self.handle, N)
+
+    def plan(self, N: int) -> str:
+        return usp_plan(self.handle, N)
 
     def make_workspace(self, N: int) -> torch.Tensor | None:
         n = self.workspace_size(N)

@@ -41,6 +41,8 @@ def test_argument_errors_without_device(usp):
     p = ctypes.c_void_p
     assert lib.usp_free(None) == 0
     assert lib.usp_workspace_size(None, 16) == 0
+    buf = ctypes.create_string_buffer(64)
+    assert lib.usp_plan(None, 16, buf, 64) == 1
     info = usp.usp_info_t()
     assert lib.usp_info(None, ctypes.byref(info)) == 1
     assert "invalid" in usp.usp_last_error()

@@ -550,3 +550,40 @@ def test_graph_capture_replays(torch, usp, M, K, N):
         RB = (M + 15) // 16
         assert int(ws[: 16 * ((RB + 3) // 4)].count_nonzero().item()) == 0
     A.free()
+
+
+# The planner's routes on MI355X (256 CUs), one per rule it documents: the row
+# kernel for few row blocks with few column tiles or few tokens; the
+# column-chunk kernel for small layers at 9-16 tokens unless a row block would
+# split into more than 8 chunks; the direct-to-LDS kernel for large layers up to
+# 256 tokens (token groups above 64; at 3-4 blocks only if no row set splits
+# over more than 4 wavefronts); the four-wavefront kernel otherwise, in passes
+# above 256 tokens. The route depends only on the shape, the token count and
+# the largest record, so a 50% Bernoulli mask over constant weights stands in.
+ROUTES = [
+    ((1024, 1024, 16), "row"), ((3584, 8192, 8), "row"),
+    ((5120, 5120, 16), "chunk S=5"), ((5120, 5120, 8), "chunk S=5"), ((13824, 5120, 16), "chunk S=5"),
+    ((3584, 8192, 16), "chunk S=8"),
+    ((5120, 13824, 16), "fourwave passes=1 nt=1"), ((5120, 5120, 32), "fourwave passes=1 nt=2"),
+    ((4101, 1000, 48), "fourwave passes=1 nt=3"), ((4101, 1000, 200), "fourwave passes=2 nt=8"),
+    ((8192, 28672, 64), "fourwave passes=1 nt=4"), ((36880, 8088, 300), "fourwave passes=5 nt=4"),
+    ((36880, 8088, 16), "dma nb=1 tg=1"), ((36880, 8088, 32), "dma nb=2 tg=1"),
+    ((36880, 8088, 64), "dma nb=4 tg=1"), ((36880, 8088, 100), "dma nb=4 tg=2"),
+    ((8192, 28672, 128), "dma nb=4 tg=2"),
+]
+
+
+def test_planner_routes(torch, usp):
+    rng = np.random.default_rng(11)
+    cache = {}
+    got = []
+    for (M, K, N), want in ROUTES:
+        if (M, K) not in cache:
+            W = np.full((M, K), 0x3C00, dtype=np.uint16)
+            mask = (rng.random((M, K), dtype=np.float32) < 0.5).astype(np.uint8)
+            cache[(M, K)] = usp.SparseMatrix(W, mask)
+        plan = cache[(M, K)].plan(N)
+        got.append(((M, K, N), plan))
+        assert plan.startswith(want), got
+    for A in cache.values():
+        A.free()
