@@ -689,8 +689,8 @@ __device__ inline void decode_record(lds_u32 *slot, const uint8_t *lut, uint2 ms
 // ---------------------------------------------------------------------------
 // Column-chunk kernel for small matrices (up to 16 tokens).
 //
-// A workgroup of four wavefronts takes four consecutive row blocks and a chunk
-// of C consecutive column tiles. The chunk's X columns (16 tokens x 256 C
+// A workgroup of W wavefronts (4 or 8) takes W consecutive row blocks and a
+// chunk of C consecutive column tiles. The chunk's X columns (16 tokens x 256 C
 // halfs) are staged in LDS once, behind the kernel's only barrier. Each
 // wavefront reads the offsets of its C records with one vector load and issues
 // the loads of all C records before decoding the first: on layers this small a
@@ -705,19 +705,19 @@ __device__ inline void decode_record(lds_u32 *slot, const uint8_t *lut, uint2 ms
 constexpr int kChunkTiles = 4;                             // C
 constexpr int kChunkXRow = kChunkTiles * kTileK * 2 + 16;  // padded token row of the chunk's X (bytes)
 
-template <int L>
-__global__ __launch_bounds__(kThreads, 2) void spmm_chunk_kernel(WaveArgs a, const uint32_t *__restrict__ off,
+template <int L, int W>
+__global__ __launch_bounds__(W * kLanes) void spmm_chunk_kernel(WaveArgs a, const uint32_t *__restrict__ off,
                                                                  const uint8_t *__restrict__ stream) {
     constexpr int C = kChunkTiles;
     constexpr int kRegion = 1024 * L + 16;  // staged values + the decode's 12-byte overread
-    constexpr int kXLoads = 16 * 32 * C / kThreads;  // 16-byte X chunks per thread
+    constexpr int kXLoads = 16 * 32 * C / (W * kLanes);  // 16-byte X chunks per thread
     __shared__ __attribute__((aligned(16))) uint8_t xs[16 * kChunkXRow];
-    __shared__ __attribute__((aligned(16))) uint8_t regions[kWaves * kRegion];
+    __shared__ __attribute__((aligned(16))) uint8_t regions[W * kRegion];
     __shared__ __attribute__((aligned(16))) uint8_t lut[16 * 8];
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int64_t S = a.maxseg;  // chunks per row block
     const int64_t rg = blockIdx.x / S, seg = blockIdx.x % S;
-    const int64_t rb = rg * kWaves + wave, kt0 = seg * C;
+    const int64_t rb = rg * W + wave, kt0 = seg * C;
     const int nct = (int)(a.KT - kt0 < C ? a.KT - kt0 : C);
 
     // X of the chunk: token n, 16-byte chunk c of its C * 256 columns; zero for
@@ -727,7 +727,7 @@ __global__ __launch_bounds__(kThreads, 2) void spmm_chunk_kernel(WaveArgs a, con
     v4u32 xv[kXLoads];
 #pragma unroll
     for (int i = 0; i < kXLoads; ++i) {
-        const int q = tid + kThreads * i, n = q / (32 * C), c = q % (32 * C);
+        const int q = tid + W * kLanes * i, n = q / (32 * C), c = q % (32 * C);
         const int64_t col = kt0 * kTileK + 8 * c;
         const int at = (n < a.N && col < a.K) ? (int)((n * a.ldx + col) * 2) : (int)a.x_bytes;
         xv[i] = __builtin_amdgcn_raw_buffer_load_b128(xr, at, 0, 0);
@@ -740,7 +740,7 @@ __global__ __launch_bounds__(kThreads, 2) void spmm_chunk_kernel(WaveArgs a, con
         __builtin_amdgcn_raw_buffer_load_b32(offr, real ? (int)((rb * a.KT + kt0 + lane) * 4) : 0x7FFFFFF0, 0, 0);
 #pragma unroll
     for (int i = 0; i < kXLoads; ++i) {
-        const int q = tid + kThreads * i, n = q / (32 * C), c = q % (32 * C);
+        const int q = tid + W * kLanes * i, n = q / (32 * C), c = q % (32 * C);
         *reinterpret_cast<v4u32 *>(xs + n * kChunkXRow + 16 * c) = xv[i];
     }
     if (tid < 16) reinterpret_cast<uint2 *>(lut)[tid] = nibble_selectors((uint32_t)tid);
@@ -1300,16 +1300,37 @@ static WaveKernelFn dma_kernel(int loads, int nb) {
 #undef USP_BY_LOADS
 }
 
-static WaveKernelFn chunk_kernel(int loads) {
-    switch (loads) {
-        case 2: return spmm_chunk_kernel<2>;
-        case 3: return spmm_chunk_kernel<3>;
-        case 4: return spmm_chunk_kernel<4>;
-        case 5: return spmm_chunk_kernel<5>;
-        case 6: return spmm_chunk_kernel<6>;
-        case 7: return spmm_chunk_kernel<7>;
-        default: return spmm_chunk_kernel<8>;
+static WaveKernelFn chunk_kernel(int loads, int wpg) {
+#define USP_CHUNK(WV)                                 \
+    switch (loads) {                                  \
+        case 2: return spmm_chunk_kernel<2, WV>;      \
+        case 3: return spmm_chunk_kernel<3, WV>;      \
+        case 4: return spmm_chunk_kernel<4, WV>;      \
+        case 5: return spmm_chunk_kernel<5, WV>;      \
+        case 6: return spmm_chunk_kernel<6, WV>;      \
+        case 7: return spmm_chunk_kernel<7, WV>;      \
+        default: return spmm_chunk_kernel<8, WV>;     \
     }
+    if (wpg == 8) {
+        USP_CHUNK(8)
+    }
+    USP_CHUNK(4)
+#undef USP_CHUNK
+}
+
+// Workgroups of the column-chunk kernel resident per CU.
+static int resident_chunk_groups(int loads, int wpg) {
+    static int cached[9][9] = {};
+    int &c = cached[loads][wpg];
+    if (c == 0) {
+        int n = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, chunk_kernel(loads, wpg), kLanes * wpg, 0) !=
+                hipSuccess ||
+            n < 1)
+            n = 1;
+        c = n;
+    }
+    return c;
 }
 
 // Wavefronts of the direct-to-LDS kernel resident per CU (queried once per
@@ -1330,6 +1351,7 @@ static int resident_waves(int loads, int nb) {
 struct WavePlan {
     WaveKind kind;
     int loads, rows, nb, tg;  // record load groups; row blocks per unit; token blocks per wavefront; groups
+    int wpg;                  // column-chunk kernel: wavefronts (row blocks) per workgroup
     int64_t sets, units, ranges, grid, maxseg;  // ranges of units; workgroups = ranges * tg
     bool split;
 };
@@ -1380,14 +1402,21 @@ static WavePlan plan_wave(const usp_matrix *A, int64_t N) {
     WavePlan p;
     p.loads = wave_loads(A);
     p.kind = wave_kind(A, p.loads, N);
-    if (p.kind == kWaveChunk) {  // workgroups of 4 row blocks x kChunkTiles column tiles
+    p.wpg = 0;
+    if (p.kind == kWaveChunk) {  // workgroups of wpg row blocks x kChunkTiles column tiles
         p.rows = 1;
         p.nb = 1;
         p.tg = 1;
         p.sets = A->RB;
         p.units = A->RB * A->KT;
         p.maxseg = ceil_div(A->KT, kChunkTiles);
-        p.ranges = ceil_div(A->RB, kWaves) * p.maxseg;
+        // 8 row blocks per workgroup when every workgroup is resident at once
+        // (the chunk's X is staged once for twice the records; 13B attention at
+        // 16 tokens: 13.1 against 13.6 us), else 4 (13B FFN up: 540 workgroups
+        // of 8 need two rounds, 28.5 against 24.5 us).
+        const int64_t cus = A->num_cus > 0 ? A->num_cus : 256;
+        p.wpg = ceil_div(A->RB, 8) * p.maxseg <= cus * resident_chunk_groups(p.loads, 8) ? 8 : 4;
+        p.ranges = ceil_div(A->RB, p.wpg) * p.maxseg;
         p.grid = p.ranges;
         p.split = p.maxseg > 1;
         return p;
@@ -1441,7 +1470,7 @@ std::string describe_plan(const usp_matrix *A, int64_t N) {
         } else {
             const WavePlan p = plan_wave(A, N);
             if (kind == kWaveChunk)
-                snprintf(buf, sizeof buf, "chunk S=%lld grid=%lld", (long long)p.maxseg, (long long)p.grid);
+                snprintf(buf, sizeof buf, "chunk S=%lld W=%d grid=%lld", (long long)p.maxseg, p.wpg, (long long)p.grid);
             else
                 snprintf(buf, sizeof buf, "dma nb=%d tg=%d grid=%lld", p.nb, p.tg, (long long)p.grid);
         }
@@ -1548,8 +1577,8 @@ static int launch_wave(const usp_matrix *A, const void *X, int64_t ldx, void *Y,
     a.tg = p.tg;
     set_epilogue(a, ep);
     if (p.kind == kWaveChunk)
-        hipLaunchKernelGGL(chunk_kernel(p.loads), dim3((unsigned)p.grid), dim3(kThreads), 0, st, a, A->d_off,
-                           reinterpret_cast<const uint8_t *>(A->d_stream));
+        hipLaunchKernelGGL(chunk_kernel(p.loads, p.wpg), dim3((unsigned)p.grid), dim3(kLanes * p.wpg), 0, st, a,
+                           A->d_off, reinterpret_cast<const uint8_t *>(A->d_stream));
     else
         hipLaunchKernelGGL(dma_kernel(p.loads, p.nb), dim3((unsigned)p.grid), dim3(kLanes), 0, st, a, A->d_off,
                            reinterpret_cast<const uint8_t *>(A->d_stream));

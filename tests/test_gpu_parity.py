@@ -560,10 +560,12 @@ def test_graph_capture_replays(torch, usp, M, K, N):
 # over more than 4 wavefronts); the four-wavefront kernel otherwise, in passes
 # above 256 tokens. The route depends only on the shape, the token count and
 # the largest record, so a 50% Bernoulli mask over constant weights stands in.
+# The column-chunk kernel takes 8 row blocks per workgroup when all its
+# workgroups are resident at once, else 4.
 ROUTES = [
     ((1024, 1024, 16), "row"), ((3584, 8192, 8), "row"),
-    ((5120, 5120, 16), "chunk S=5"), ((5120, 5120, 8), "chunk S=5"), ((13824, 5120, 16), "chunk S=5"),
-    ((3584, 8192, 16), "chunk S=8"),
+    ((5120, 5120, 16), "chunk S=5 W=8"), ((5120, 5120, 8), "chunk S=5 W=8"), ((13824, 5120, 16), "chunk S=5 W=4"),
+    ((3584, 8192, 16), "chunk S=8 W=8"),
     ((5120, 13824, 16), "fourwave passes=1 nt=1"), ((5120, 5120, 32), "fourwave passes=1 nt=2"),
     ((4101, 1000, 48), "fourwave passes=1 nt=3"), ((4101, 1000, 200), "fourwave passes=2 nt=8"),
     ((8192, 28672, 64), "fourwave passes=1 nt=4"), ((36880, 8088, 300), "fourwave passes=5 nt=4"),
