@@ -589,3 +589,29 @@ def test_planner_routes(torch, usp):
         assert plan.startswith(want), got
     for A in cache.values():
         A.free()
+
+
+# Random shapes (fixed seeds): M, K from 1 to several thousand, N from 1 to 300,
+# densities from 0 to 1, through whatever kernel the planner picks; exact on
+# small integers, every output. Each case prints its shape and route first.
+def _random_cases(count=32, seed=2607):
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(count):
+        M = int(rng.choice([1, 7, 16, 33, 250, 1023, 2049, 4101, 6000, 9000]))
+        K = int(rng.choice([1, 9, 255, 256, 512, 704, 1504, 3000, 5120]))  # mostly multiples of 8
+        N = int(rng.choice([1, 3, 8, 16, 17, 31, 48, 64, 65, 100, 129, 256, 300]))
+        d = float(rng.choice([0.0, 0.05, 0.3, 0.5, 0.7, 1.0]))
+        out.append((M, K, N, d, 100 + i))
+    return out
+
+
+@pytest.mark.parametrize("M,K,N,density,seed", _random_cases())
+def test_random_shapes_exact(torch, usp, M, K, N, density, seed):
+    W, mask, X = wl.make_small_int(M, K, N, density, seed=seed, lo=-1, hi=1)
+    A = usp.SparseMatrix(W, mask)
+    print(f"case M={M} K={K} N={N} density={density}: {A.plan(N)}", flush=True)
+    A.free()
+    Y = run(torch, usp, W, mask, X)
+    Yref, _ = oracle.masked_gemm(W, mask, X)
+    assert np.array_equal(Y, Yref)
