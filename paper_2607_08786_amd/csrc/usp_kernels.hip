@@ -53,6 +53,7 @@ constexpr int kCachePolicyDevice = 16;
 
 constexpr int kWaves = 4;                              // row blocks per workgroup
 constexpr int kThreads = kWaves * kLanes;              // 256
+constexpr int kGroupRows = kWaves * kTileRows;         // rows of a row group (64)
 constexpr int kWRegionBytes = kMaxValBytes;            // 8 KB per wavefront (8 KB aligned)
 constexpr int kXRowBytes = kTileK * 2 + 16;            // 528: padded token row of the X tile
 constexpr int kMaxNT = 8;                              // 16-token blocks per pass (N <= 128)
@@ -285,9 +286,13 @@ __device__ inline void store_y4(const SpmmArgs &a, int n, int64_t m, float v0, f
 
 // Registers holding one prefetched tile: this lane's share of the X tile and of
 // the wavefront's tile record.
+// 16-byte chunks of an X tile of NT blocks of 16 tokens per thread.
+template <int NT>
+constexpr int kXTileChunks = NT * 16 * 32 / kThreads;
+
 template <int NT>
 struct TileRegs {
-    uint4 x[2 * NT];
+    uint4 x[kXTileChunks<NT>];
     uint4 w[8];
     uint2 msk;
     int nch;  // 16-byte chunks of packed values (wavefront-uniform)
@@ -303,7 +308,7 @@ __device__ inline void fetch_tile(const SpmmArgs &a, const uint32_t *__restrict_
                                   const uint8_t *__restrict__ stream, int64_t rb, bool rb_ok, int64_t kt, int tid,
                                   int lane, TileRegs<NT> &r) {
 #pragma unroll
-    for (int i = 0; i < 2 * NT; ++i) {
+    for (int i = 0; i < kXTileChunks<NT>; ++i) {
         const int c = tid + kThreads * i;
         r.x[i] = load_x_chunk<XFAST>(a, c >> 5, kt * kTileK + 8 * (c & 31));
     }
@@ -325,7 +330,7 @@ __device__ inline int64_t unit_owner(int64_t x, int64_t U, int64_t G) { return (
 template <int NT>
 __device__ inline void stage_tile(const TileRegs<NT> &r, uint8_t *xs, uint8_t *region, int tid, int lane) {
 #pragma unroll
-    for (int i = 0; i < 2 * NT; ++i) {
+    for (int i = 0; i < kXTileChunks<NT>; ++i) {
         const int c = tid + kThreads * i;
         *reinterpret_cast<uint4 *>(xs + (c >> 5) * kXRowBytes + 16 * (c & 31)) = r.x[i];
     }
@@ -376,10 +381,10 @@ __device__ inline void flush_row_group(const SpmmArgs &a, int64_t rg, int64_t wg
         return;
     }
     const int64_t nseg = w_last - w_first + 1;
-    // Partials of this row group: [slot][token][64 rows] fp32, accessed through a
+    // Partials of this row group: [slot][token][kGroupRows rows] fp32, accessed through a
     // buffer resource with device-scope (sc1) cache policy: stores are written
     // through to the device-coherent level, loads read it.
-    const int64_t slot_floats = (int64_t)a.N * 64;
+    const int64_t slot_floats = (int64_t)a.N * kGroupRows;
     float *slot0 = a.ws + rg * a.maxseg * slot_floats;
     const __amdgpu_buffer_rsrc_t part =
         __builtin_amdgcn_make_buffer_rsrc(slot0, (short)0, (int)(nseg * slot_floats * 4), kBufferRsrcWord3);
@@ -389,7 +394,7 @@ __device__ inline void flush_row_group(const SpmmArgs &a, int64_t rg, int64_t wg
     for (int nb = 0; nb < NT; ++nb) {
         const int n = 16 * nb + (lane & 15);
         if (n >= a.N) continue;
-        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, acc[nb]), part, mine + (n * 64 + r0) * 4, 0,
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, acc[nb]), part, mine + (n * kGroupRows + r0) * 4, 0,
                                                kCachePolicyDevice);
     }
     __builtin_amdgcn_s_waitcnt(0);  // every partial store acknowledged before the arrival is counted
@@ -403,9 +408,10 @@ __device__ inline void flush_row_group(const SpmmArgs &a, int64_t rg, int64_t wg
     __syncthreads();  // the flag may be reused by the next flush
     if (!last) return;
     const int64_t row0 = rg * kWaves * kTileRows;
-    for (int e = tid; e < 16 * a.N; e += kThreads) {  // 4 consecutive rows of one token per item
-        const int n = e >> 4;
-        const int r = 4 * (e & 15);
+    constexpr int kItems = kGroupRows / 4;  // items of 4 consecutive rows per token
+    for (int e = tid; e < kItems * a.N; e += kThreads) {
+        const int n = e / kItems;
+        const int r = 4 * (e % kItems);
         if (row0 + r >= a.RB * kTileRows) continue;
         floatx4 sum = {0.f, 0.f, 0.f, 0.f};
         for (int64_t j0 = 0; j0 < nseg; j0 += 8) {
@@ -415,7 +421,7 @@ __device__ inline void flush_row_group(const SpmmArgs &a, int64_t rg, int64_t wg
 #pragma unroll
             for (int jj = 0; jj < 8; ++jj)
                 v[jj] = j0 + jj < nseg ? __builtin_amdgcn_raw_buffer_load_b128(
-                                             part, (int)((j0 + jj) * slot_floats * 4) + (n * 64 + r) * 4, 0,
+                                             part, (int)((j0 + jj) * slot_floats * 4) + (n * kGroupRows + r) * 4, 0,
                                              kCachePolicyDevice)
                                        : v4u32{0u, 0u, 0u, 0u};
 #pragma unroll
@@ -428,7 +434,7 @@ __device__ inline void flush_row_group(const SpmmArgs &a, int64_t rg, int64_t wg
 }
 
 template <int NT, bool XFAST>
-__global__ __launch_bounds__(kThreads, 2) void spmm_kernel(SpmmArgs a, const uint32_t *__restrict__ off,
+__global__ __launch_bounds__(kThreads, 8 / kWaves) void spmm_kernel(SpmmArgs a, const uint32_t *__restrict__ off,
                                                                    const uint8_t *__restrict__ stream) {
     // Wavefront regions first, 8 KB each, so a region offset can be masked; the
     // last region gets 16 bytes of read slack.
@@ -1499,7 +1505,7 @@ static size_t counters_bytes(const usp_matrix *A) {
 }
 
 static size_t partials_bytes(const SpmmPlan &p, int64_t nb) {
-    return (size_t)p.row_groups * (size_t)p.maxseg * (size_t)nb * 64 * sizeof(float);
+    return (size_t)p.row_groups * (size_t)p.maxseg * (size_t)nb * kGroupRows * sizeof(float);
 }
 
 static size_t wave_partials_bytes(const usp_matrix *A, int64_t N) {
