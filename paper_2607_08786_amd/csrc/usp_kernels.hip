@@ -6,8 +6,8 @@
 //     workgroup streams a contiguous range of units (4 row blocks x 1 column
 //     tile), records moved straight into a ring of LDS slots, X in registers;
 //     more than 4 blocks of 16 tokens are split into token groups;
-//   * spmm_chunk_kernel (small layers, up to 16 tokens): 4 row blocks x a chunk
-//     of 4 column tiles per workgroup, every record requested at once;
+//   * spmm_chunk_kernel (small layers, up to 16 tokens): 4 or 8 row blocks x a
+//     chunk of 4 column tiles per workgroup, every record requested at once;
 //   * spmm_row_kernel (few row blocks, up to 16 tokens): one row block per
 //     workgroup, its column tiles split over the wavefronts and summed in LDS;
 //   * spmm_kernel (everything else, any token count in passes): a workgroup of
