@@ -34,6 +34,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdio>
 #include <string>
 
@@ -1139,18 +1140,25 @@ __global__ __launch_bounds__(64) void densify_kernel(const uint8_t *stream, cons
 
 }  // namespace
 
+// Resident workgroups per CU of a kernel, queried from the runtime once and kept
+// in `slot`. Host threads planning calls at the same time may both query; they
+// store the same value, and the slot is atomic, so that is not a data race.
+static int cached_occupancy(std::atomic<int> &slot, const void *kernel, int threads) {
+    int c = slot.load(std::memory_order_relaxed);
+    if (c == 0) {
+        int n = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, threads, 0) != hipSuccess || n < 1) n = 1;
+        slot.store(n, std::memory_order_relaxed);
+        c = n;
+    }
+    return c;
+}
+
 // Workgroups of spmm_kernel<NT, XFAST> resident per CU (queried once per instance).
 template <int NT, bool XFAST>
 static int resident_wgs() {
-    static int cached = 0;
-    if (cached == 0) {
-        int n = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, spmm_kernel<NT, XFAST>, kThreads, 0) != hipSuccess ||
-            n < 1)
-            n = 1;
-        cached = n;
-    }
-    return cached;
+    static std::atomic<int> cached{0};
+    return cached_occupancy(cached, reinterpret_cast<const void *>(spmm_kernel<NT, XFAST>), kThreads);
 }
 
 // Token blocks the four-wavefront kernel is built for: 1-4, and 8 for 5-8.
@@ -1261,16 +1269,8 @@ static WaveKernelFn row_kernel(int loads, int wpg) {
 
 // Workgroups of the row-block kernel resident per CU.
 static int resident_row_groups(int loads, int wpg) {
-    static int cached[9][9] = {};
-    int &c = cached[loads][wpg];
-    if (c == 0) {
-        int n = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, row_kernel(loads, wpg), kLanes * wpg, 0) != hipSuccess ||
-            n < 1)
-            n = 1;
-        c = n;
-    }
-    return c;
+    static std::atomic<int> cached[9][9];
+    return cached_occupancy(cached[loads][wpg], reinterpret_cast<const void *>(row_kernel(loads, wpg)), kLanes * wpg);
 }
 
 // The most wavefronts per row block (2, 4, 5 or 8, at most KT) for which every
@@ -1326,32 +1326,15 @@ static WaveKernelFn chunk_kernel(int loads, int wpg) {
 
 // Workgroups of the column-chunk kernel resident per CU.
 static int resident_chunk_groups(int loads, int wpg) {
-    static int cached[9][9] = {};
-    int &c = cached[loads][wpg];
-    if (c == 0) {
-        int n = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, chunk_kernel(loads, wpg), kLanes * wpg, 0) !=
-                hipSuccess ||
-            n < 1)
-            n = 1;
-        c = n;
-    }
-    return c;
+    static std::atomic<int> cached[9][9];
+    return cached_occupancy(cached[loads][wpg], reinterpret_cast<const void *>(chunk_kernel(loads, wpg)), kLanes * wpg);
 }
 
 // Wavefronts of the direct-to-LDS kernel resident per CU (queried once per
 // variant).
 static int resident_waves(int loads, int nb) {
-    static int cached[9][kMaxDmaTokenBlocks + 1] = {};
-    int &c = cached[loads][nb];
-    if (c == 0) {
-        int n = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dma_kernel(loads, nb), kLanes, 0) != hipSuccess ||
-            n < 1)
-            n = 1;
-        c = n;
-    }
-    return c;
+    static std::atomic<int> cached[9][kMaxDmaTokenBlocks + 1];
+    return cached_occupancy(cached[loads][nb], reinterpret_cast<const void *>(dma_kernel(loads, nb)), kLanes);
 }
 
 struct WavePlan {
