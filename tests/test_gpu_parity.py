@@ -615,3 +615,42 @@ def test_random_shapes_exact(torch, usp, M, K, N, density, seed):
     Y = run(torch, usp, W, mask, X)
     Yref, _ = oracle.masked_gemm(W, mask, X)
     assert np.array_equal(Y, Yref)
+
+
+# Concurrent host threads, each with its own handle, stream and workspace (the
+# contract for concurrent calls), ten products each through the planner's
+# different kernels; every result equals the single-threaded one bit for bit.
+def test_concurrent_host_threads(torch, usp):
+    import threading
+    shapes = [(5120, 2048, 16), (4101, 1000, 48), (1024, 1024, 16), (36880, 8088, 16)]
+    cases = []
+    for i, (M, K, N) in enumerate(shapes):
+        W, mask, X = wl.make_random(M, K, N, 0.5, seed=300 + i)
+        A = usp.SparseMatrix(W, mask)
+        Xd = to_dev(torch, X)
+        ref = A.spmm(Xd)
+        cases.append((A, Xd, ref))
+    torch.cuda.synchronize()
+    errors = []
+
+    def work(A, Xd, ref):
+        try:
+            st = torch.cuda.Stream()
+            ws = A.make_workspace(Xd.shape[0])
+            with torch.cuda.stream(st):
+                for _ in range(10):
+                    Y = A.spmm(Xd, workspace=ws)
+            st.synchronize()
+            if not torch.equal(Y, ref):
+                errors.append((A.M, A.K))
+        except Exception as e:  # reported below
+            errors.append(repr(e))
+
+    threads = [threading.Thread(target=work, args=c) for c in cases]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    for A, _, _ in cases:
+        A.free()
+    assert not errors, errors
