@@ -6,7 +6,7 @@
 //     workgroup streams a contiguous range of units (4 row blocks x 1 column
 //     tile), records moved straight into a ring of LDS slots, X in registers;
 //     more than 4 blocks of 16 tokens are split into token groups;
-//   * spmm_chunk_kernel (small layers, up to 16 tokens): 4 or 8 row blocks x a
+//   * spmm_chunk_kernel (small layers, up to 32 tokens): 4 or 8 row blocks x a
 //     chunk of 4 column tiles per workgroup, every record requested at once;
 //   * spmm_row_kernel (few row blocks, up to 16 tokens): one row block per
 //     workgroup, its column tiles split over the wavefronts and summed in LDS;
@@ -694,11 +694,12 @@ __device__ inline void decode_record(lds_u32 *slot, const uint8_t *lut, uint2 ms
 }
 
 // ---------------------------------------------------------------------------
-// Column-chunk kernel for small matrices (up to 16 tokens).
+// Column-chunk kernel for small matrices (up to 32 tokens).
 //
 // A workgroup of W wavefronts (4 or 8) takes W consecutive row blocks and a
-// chunk of C consecutive column tiles. The chunk's X columns (16 tokens x 256 C
-// halfs) are staged in LDS once, behind the kernel's only barrier. Each
+// chunk of C consecutive column tiles. The chunk's X columns (NB blocks of 16
+// tokens x 256 C halfs) are staged in LDS once, behind the kernel's only
+// barrier; every decoded step feeds NB MFMAs. Each
 // wavefront reads the offsets of its C records with one vector load and issues
 // the loads of all C records before decoding the first: on layers this small a
 // wavefront has only a few records, and their round trips, not the HBM rate,
@@ -710,15 +711,16 @@ __device__ inline void decode_record(lds_u32 *slot, const uint8_t *lut, uint2 ms
 // ---------------------------------------------------------------------------
 
 constexpr int kChunkTiles = 4;                             // C
+constexpr int kMaxChunkTokenBlocks = 2;                    // NB
 constexpr int kChunkXRow = kChunkTiles * kTileK * 2 + 16;  // padded token row of the chunk's X (bytes)
 
-template <int L, int W>
+template <int L, int W, int NB>
 __global__ __launch_bounds__(W * kLanes) void spmm_chunk_kernel(WaveArgs a, const uint32_t *__restrict__ off,
                                                                  const uint8_t *__restrict__ stream) {
     constexpr int C = kChunkTiles;
     constexpr int kRegion = 1024 * L + 16;  // staged values + the decode's 12-byte overread
-    constexpr int kXLoads = 16 * 32 * C / (W * kLanes);  // 16-byte X chunks per thread
-    __shared__ __attribute__((aligned(16))) uint8_t xs[16 * kChunkXRow];
+    constexpr int kXLoads = NB * 16 * 32 * C / (W * kLanes);  // 16-byte X chunks per thread
+    __shared__ __attribute__((aligned(16))) uint8_t xs[NB * 16 * kChunkXRow];
     __shared__ __attribute__((aligned(16))) uint8_t regions[W * kRegion];
     __shared__ __attribute__((aligned(16))) uint8_t lut[16 * 8];
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -768,33 +770,43 @@ __global__ __launch_bounds__(W * kLanes) void spmm_chunk_kernel(WaveArgs a, cons
     lds_u32 *const rbase = as_lds(region);
     const int n_lane = lane & 15, g4 = 4 * (lane >> 4);
     const uint8_t *const xrow = xs + n_lane * kChunkXRow + 2 * 8 * (lane >> 4);
-    floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
+    floatx4 acc[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int j = 0; j < C; ++j) {
         if (j < nct) {
             // In-order LDS: the previous decode's reads of the region are done.
 #pragma unroll
             for (int i = 0; i < L; ++i) reinterpret_cast<v4u32 *>(region)[lane + kLanes * i] = rec[j].w[i];
-            v4u32 xb[1][kSteps];
+            v4u32 xb[NB][kSteps];
 #pragma unroll
-            for (int s = 0; s < kSteps; ++s)
-                xb[0][s] = *reinterpret_cast<const v4u32 *>(xrow + 2 * (j * kTileK + 32 * s));
-            decode_record<1>(rbase, lut, rec[j].msk, xb, reinterpret_cast<floatx4(&)[1]>(acc));
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int s = 0; s < kSteps; ++s)
+                    xb[nb][s] = *reinterpret_cast<const v4u32 *>(xrow + nb * 16 * kChunkXRow + 2 * (j * kTileK + 32 * s));
+            decode_record<NB>(rbase, lut, rec[j].msk, xb, acc);
         }
     }
     if (S == 1) {
-        if (n_lane < a.N) store_rows4(a, n_lane, rb * kTileRows + g4, acc);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+            if (16 * nb + n_lane < a.N) store_rows4(a, 16 * nb + n_lane, rb * kTileRows + g4, acc[nb]);
         return;
     }
     const int64_t slot_floats = (int64_t)a.N * kTileRows;
     float *slot = a.ws + (rb * S + seg) * slot_floats;
     const __amdgpu_buffer_rsrc_t part =
         __builtin_amdgcn_make_buffer_rsrc(slot, (short)0, (int)(slot_floats * 4), kBufferRsrcWord3);
-    if (n_lane < a.N)
-        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, acc), part, (n_lane * kTileRows + g4) * 4, 0,
-                                               kCachePolicyDevice);
-    __builtin_amdgcn_s_waitcnt(0);  // the partial is acknowledged before the arrival counts
-    arrive_row_set<1>(a, rb, S, lane);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+        const int n = 16 * nb + n_lane;
+        if (n < a.N)
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, acc[nb]), part, (n * kTileRows + g4) * 4,
+                                                   0, kCachePolicyDevice);
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // the partials are acknowledged before the arrival counts
+    arrive_row_set<1, NB>(a, rb, S, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -1306,28 +1318,35 @@ static WaveKernelFn dma_kernel(int loads, int nb) {
 #undef USP_BY_LOADS
 }
 
-static WaveKernelFn chunk_kernel(int loads, int wpg) {
-#define USP_CHUNK(WV)                                 \
-    switch (loads) {                                  \
-        case 2: return spmm_chunk_kernel<2, WV>;      \
-        case 3: return spmm_chunk_kernel<3, WV>;      \
-        case 4: return spmm_chunk_kernel<4, WV>;      \
-        case 5: return spmm_chunk_kernel<5, WV>;      \
-        case 6: return spmm_chunk_kernel<6, WV>;      \
-        case 7: return spmm_chunk_kernel<7, WV>;      \
-        default: return spmm_chunk_kernel<8, WV>;     \
+static WaveKernelFn chunk_kernel(int loads, int wpg, int nb) {
+#define USP_CHUNK(WV, NBV)                                 \
+    switch (loads) {                                       \
+        case 2: return spmm_chunk_kernel<2, WV, NBV>;      \
+        case 3: return spmm_chunk_kernel<3, WV, NBV>;      \
+        case 4: return spmm_chunk_kernel<4, WV, NBV>;      \
+        case 5: return spmm_chunk_kernel<5, WV, NBV>;      \
+        case 6: return spmm_chunk_kernel<6, WV, NBV>;      \
+        case 7: return spmm_chunk_kernel<7, WV, NBV>;      \
+        default: return spmm_chunk_kernel<8, WV, NBV>;     \
+    }
+    if (nb == 1) {
+        if (wpg == 8) {
+            USP_CHUNK(8, 1)
+        }
+        USP_CHUNK(4, 1)
     }
     if (wpg == 8) {
-        USP_CHUNK(8)
+        USP_CHUNK(8, 2)
     }
-    USP_CHUNK(4)
+    USP_CHUNK(4, 2)
 #undef USP_CHUNK
 }
 
 // Workgroups of the column-chunk kernel resident per CU.
-static int resident_chunk_groups(int loads, int wpg) {
-    static std::atomic<int> cached[9][9];
-    return cached_occupancy(cached[loads][wpg], reinterpret_cast<const void *>(chunk_kernel(loads, wpg)), kLanes * wpg);
+static int resident_chunk_groups(int loads, int wpg, int nb) {
+    static std::atomic<int> cached[9][9][kMaxChunkTokenBlocks + 1];
+    return cached_occupancy(cached[loads][wpg][nb], reinterpret_cast<const void *>(chunk_kernel(loads, wpg, nb)),
+                            kLanes * wpg);
 }
 
 // Wavefronts of the direct-to-LDS kernel resident per CU (queried once per
@@ -1351,7 +1370,8 @@ struct WavePlan {
 // tokens, the row-block kernel when there are no more row blocks than CUs (its
 // workgroups then spread evenly) and otherwise the column-chunk kernel (13B
 // attention, 13B FFN up) unless a row block would be split into more than 8
-// chunks (13B FFN down: 14 chunks, 29.0 against 27.7 us); everything else goes
+// chunks (13B FFN down: 14 chunks, 29.0 against 27.7 us); the column-chunk
+// kernel also at 17 to 32 tokens on the conditions below; everything else goes
 // to the four-wavefront kernel, which shares X through LDS.
 constexpr int64_t kDmaUnitsPerSlot = 8;
 constexpr int64_t kMaxDmaWideSplit = 4;
@@ -1382,8 +1402,17 @@ static WaveKind wave_kind(const usp_matrix *A, int loads, int64_t N) {
     if (nb == 1 && A->RB * A->KT <= kSmallMaxTiles && A->RB <= (A->num_cus > 0 ? A->num_cus : 256) &&
         (A->KT <= kRowMaxTiles || N <= 8))
         return kWaveRow;
-    if (nb == 1 && A->RB * A->KT <= kChunkMaxTiles && ceil_div(A->KT, kChunkTiles) <= kChunkMaxSplit)
-        return kWaveChunk;
+    if (nb <= kMaxChunkTokenBlocks && A->RB * A->KT <= kChunkMaxTiles && ceil_div(A->KT, kChunkTiles) <= kChunkMaxSplit) {
+        if (nb == 1) return kWaveChunk;
+        // Two token blocks (one workgroup per CU: X for 32 tokens in LDS) only
+        // in a single round of workgroups of 8 row blocks that covers at least
+        // half the CUs: 13B attention 15.8 against 18.4 us at 32 tokens, one
+        // GPU's share of the 70B FFN 16.5 against 22.0; the 13B FFN up (1080
+        // workgroups of 4) 49.8 against 33.2, the tiny layer (8) 10.2 against 7.8.
+        const int64_t cus = A->num_cus > 0 ? A->num_cus : 256;
+        const int64_t wgs = ceil_div(A->RB, 8) * ceil_div(A->KT, kChunkTiles);
+        if (2 * wgs >= cus && wgs <= cus * resident_chunk_groups(loads, 8, nb)) return kWaveChunk;
+    }
     return kWaveNone;
 }
 
@@ -1394,7 +1423,7 @@ static WavePlan plan_wave(const usp_matrix *A, int64_t N) {
     p.wpg = 0;
     if (p.kind == kWaveChunk) {  // workgroups of wpg row blocks x kChunkTiles column tiles
         p.rows = 1;
-        p.nb = 1;
+        p.nb = (int)ceil_div(N, 16);
         p.tg = 1;
         p.sets = A->RB;
         p.units = A->RB * A->KT;
@@ -1404,7 +1433,7 @@ static WavePlan plan_wave(const usp_matrix *A, int64_t N) {
         // 16 tokens: 13.1 against 13.6 us), else 4 (13B FFN up: 540 workgroups
         // of 8 need two rounds, 28.5 against 24.5 us).
         const int64_t cus = A->num_cus > 0 ? A->num_cus : 256;
-        p.wpg = ceil_div(A->RB, 8) * p.maxseg <= cus * resident_chunk_groups(p.loads, 8) ? 8 : 4;
+        p.wpg = ceil_div(A->RB, 8) * p.maxseg <= cus * resident_chunk_groups(p.loads, 8, p.nb) ? 8 : 4;
         p.ranges = ceil_div(A->RB, p.wpg) * p.maxseg;
         p.grid = p.ranges;
         p.split = p.maxseg > 1;
@@ -1459,7 +1488,8 @@ std::string describe_plan(const usp_matrix *A, int64_t N) {
         } else {
             const WavePlan p = plan_wave(A, N);
             if (kind == kWaveChunk)
-                snprintf(buf, sizeof buf, "chunk S=%lld W=%d grid=%lld", (long long)p.maxseg, p.wpg, (long long)p.grid);
+                snprintf(buf, sizeof buf, "chunk S=%lld W=%d nb=%d grid=%lld", (long long)p.maxseg, p.wpg, p.nb,
+                         (long long)p.grid);
             else
                 snprintf(buf, sizeof buf, "dma nb=%d tg=%d grid=%lld", p.nb, p.tg, (long long)p.grid);
         }
@@ -1566,7 +1596,7 @@ static int launch_wave(const usp_matrix *A, const void *X, int64_t ldx, void *Y,
     a.tg = p.tg;
     set_epilogue(a, ep);
     if (p.kind == kWaveChunk)
-        hipLaunchKernelGGL(chunk_kernel(p.loads, p.wpg), dim3((unsigned)p.grid), dim3(kLanes * p.wpg), 0, st, a,
+        hipLaunchKernelGGL(chunk_kernel(p.loads, p.wpg, p.nb), dim3((unsigned)p.grid), dim3(kLanes * p.wpg), 0, st, a,
                            A->d_off, reinterpret_cast<const uint8_t *>(A->d_stream));
     else
         hipLaunchKernelGGL(dma_kernel(p.loads, p.nb), dim3((unsigned)p.grid), dim3(kLanes), 0, st, a, A->d_off,

@@ -486,7 +486,7 @@ def test_many_passes_large_matrix_exact(torch, usp):
 # One GPU's share of the 70B FFN under 8-way row sharding (3584 x 8192: fewer
 # row blocks than CUs, so the K dimension is split), every output against the
 # oracle's tolerance.
-@pytest.mark.parametrize("N", [16, 64])
+@pytest.mark.parametrize("N", [16, 32, 64])
 def test_sharded_layer_full(torch, usp, N):
     inst = wl.make_instance("ffn70b_shard8", N)
     Y = run(torch, usp, inst.W, inst.mask, inst.X)
@@ -500,6 +500,33 @@ def test_chunk_kernel_many_workgroups_exact(torch, usp):
     Y = run(torch, usp, W, mask, X)
     Yref, _ = oracle.masked_gemm(W, mask, X)
     assert np.array_equal(Y, Yref)
+
+
+# Column-chunk kernel at two blocks of 16 tokens (the chunk's X for 32 tokens
+# in LDS, two MFMAs per decoded step; taken when one round of workgroups of 8
+# row blocks covers at least half the CUs): the 13B attention shape, a ragged
+# last row group with a short last chunk (15 column tiles: 4, 4, 4, 3) and
+# ragged tokens, and no split (4 column tiles, 1019 row blocks); exact on small
+# integers, every output.
+@pytest.mark.parametrize("M,K,N", [(5120, 5120, 32), (4101, 3800, 27), (16300, 1000, 17)])
+def test_chunk_kernel_two_blocks_exact(torch, usp, M, K, N):
+    W, mask, X = wl.make_small_int(M, K, N, 0.5, seed=M + 5 * K + N, lo=-1, hi=1)
+    A = usp.SparseMatrix(W, mask)
+    plan = A.plan(N)
+    A.free()
+    assert plan.startswith("chunk") and "nb=2" in plan, plan
+    Y = run(torch, usp, W, mask, X)
+    Yref, _ = oracle.masked_gemm(W, mask, X)
+    assert np.array_equal(Y, Yref)
+
+
+# Column-chunk kernel at two token blocks on random fp16 data: four chunks per
+# row block summed through the workspace, 29 tokens, every output against the
+# oracle's tolerance.
+def test_chunk_kernel_two_blocks_random_full(torch, usp):
+    W, mask, X = wl.make_random(4101, 4000, 29, 0.55, seed=27)
+    Y = run(torch, usp, W, mask, X)
+    assert_close(Y, W, mask, X)
 
 
 # Column-chunk kernel with a short last chunk: 6 column tiles (chunks of 4 and
@@ -555,10 +582,11 @@ def test_graph_capture_replays(torch, usp, M, K, N):
 # The planner's routes on MI355X (256 CUs), one per rule it documents: the row
 # kernel for few row blocks with few column tiles or few tokens; the
 # column-chunk kernel for small layers at 9-16 tokens unless a row block would
-# split into more than 8 chunks; the direct-to-LDS kernel for large layers up to
-# 256 tokens (token groups above 64; at 3-4 blocks only if no row set splits
-# over more than 4 wavefronts); the four-wavefront kernel otherwise, in passes
-# above 256 tokens. The route depends only on the shape, the token count and
+# split into more than 8 chunks, and at 17-32 tokens when one round of its
+# workgroups of 8 row blocks covers at least half the CUs; the direct-to-LDS
+# kernel for large layers up to 256 tokens (token groups above 64; at 3-4
+# blocks only if no row set splits over more than 4 wavefronts); the
+# four-wavefront kernel otherwise, in passes above 256 tokens. The route depends only on the shape, the token count and
 # the largest record, so a 50% Bernoulli mask over constant weights stands in.
 # The column-chunk kernel takes 8 row blocks per workgroup when all its
 # workgroups are resident at once, else 4.
@@ -566,7 +594,9 @@ ROUTES = [
     ((1024, 1024, 16), "row"), ((3584, 8192, 8), "row"),
     ((5120, 5120, 16), "chunk S=5 W=8"), ((5120, 5120, 8), "chunk S=5 W=8"), ((13824, 5120, 16), "chunk S=5 W=4"),
     ((3584, 8192, 16), "chunk S=8 W=8"),
-    ((5120, 13824, 16), "fourwave passes=1 nt=1"), ((5120, 5120, 32), "fourwave passes=1 nt=2"),
+    ((5120, 5120, 32), "chunk S=5 W=8 nb=2"), ((3584, 8192, 32), "chunk S=8 W=8 nb=2"),
+    ((13824, 5120, 32), "fourwave passes=1 nt=2"), ((1024, 1024, 32), "fourwave passes=1 nt=2"),
+    ((5120, 13824, 16), "fourwave passes=1 nt=1"),
     ((4101, 1000, 48), "fourwave passes=1 nt=3"), ((4101, 1000, 200), "fourwave passes=2 nt=8"),
     ((8192, 28672, 64), "fourwave passes=1 nt=4"), ((36880, 8088, 300), "fourwave passes=5 nt=4"),
     ((36880, 8088, 16), "dma nb=1 tg=1"), ((36880, 8088, 32), "dma nb=2 tg=1"),
