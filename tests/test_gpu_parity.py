@@ -317,10 +317,12 @@ def test_mid_tokens_random(torch, usp):
 # Fused epilogue (usp_spmm_ex): Y = act(W X + bias) + residual against the
 # oracle's product through the same epilogue, with the error scale carried
 # through the activation's largest slope. Every kernel: the row-block kernel
-# (1024 x 1024, 16 tokens), the column-chunk kernel (4101 x 1000, 16), the
-# four-wavefront kernel (48 tokens), the direct-to-LDS kernel (36880 x 8088:
-# 16 tokens, 27 tokens, 100 tokens in token groups).
-EPI_SMALL = [(1024, 1024, 16), (4101, 1000, 16), (4101, 1000, 48)]
+# (1024 x 1024, 16 tokens), the column-chunk kernel (4101 x 1000, 16; two
+# token blocks: 4101 x 3800 at 27 tokens, split over 4 chunks, and 16300 x
+# 1000 at 17, unsplit), the four-wavefront kernel (48 tokens), the
+# direct-to-LDS kernel (36880 x 8088: 16 tokens, 27 tokens, 100 tokens in
+# token groups).
+EPI_SMALL = [(1024, 1024, 16), (4101, 1000, 16), (4101, 3800, 27), (16300, 1000, 17), (4101, 1000, 48)]
 EPI_LARGE = [((36880, 8088, 16), "gelu_tanh"), ((36880, 8088, 27), "silu"), ((36880, 8088, 100), "relu")]
 
 
