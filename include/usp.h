@@ -127,7 +127,7 @@ usp_status usp_spmm_ex(const usp_matrix *A, const void *X, int64_t ldx, void *Y,
 
 /*
  * usp_plan -- which kernel usp_spmm runs for this handle and N when X is 16-byte
- * aligned with ldx = K, as a short text ("row W=8", "chunk S=5 grid=400",
+ * aligned with ldx = K, as a short text ("row W=8", "chunk S=5 W=8 nb=1 grid=200",
  * "dma nb=4 tg=1 grid=1024", "fourwave passes=1 nt=2 grid=768"), written to
  * buf (at most len bytes with the terminating NUL, truncated if longer). For
  * tests and tuning; enqueues nothing. USP_ERR_INVALID_ARG for a NULL handle,
