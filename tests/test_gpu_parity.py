@@ -227,7 +227,7 @@ def test_workspace_shared_between_handles(torch, usp):
 
 # Full-size workloads, sampled output rows (the oracle computes them one by one),
 # in the same launch configuration the benchmark times.
-@pytest.mark.parametrize("name,N,s", [("attn13b", 16, 50), ("attn13b", 8, 50), ("ffn13b_up", 64, 50),
+@pytest.mark.parametrize("name,N,s", [("attn13b", 16, 50), ("attn13b", 8, 50), ("attn13b", 32, 50), ("ffn13b_up", 64, 50),
                                       ("ffn13b_down", 16, 50), ("ffn70b", 16, 50), ("ffn70b", 256, 40),
                                       ("ffn70b", 32, 70), ("ffn66b", 16, 60)])
 def test_workload_sampled_rows(torch, usp, name, N, s):
