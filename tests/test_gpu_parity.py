@@ -546,11 +546,11 @@ def test_chunk_kernel_short_last_chunk_exact(torch, usp, M, K, N):
 # eager product) in between; every replay must equal the eager result bit for
 # bit. The graph holds only the library's kernels (no memset node), and split
 # products must leave their arrival counters at zero for the next replay. Every
-# kernel: row-block (1024 x 1024, 16), column-chunk (5120 x 5120, 16, 5 chunks
-# per row block), direct-to-LDS (36880 x 8088 at 16 and 100 tokens), and
-# four-wavefront (4101 x 1000, 48).
-@pytest.mark.parametrize("M,K,N", [(1024, 1024, 16), (5120, 5120, 16), (36880, 8088, 16), (36880, 8088, 100),
-                                   (4101, 1000, 48)])
+# kernel: row-block (1024 x 1024, 16), column-chunk (5120 x 5120, 16 and, with
+# two token blocks, 32; 5 chunks per row block), direct-to-LDS (36880 x 8088 at
+# 16 and 100 tokens), and four-wavefront (4101 x 1000, 48).
+@pytest.mark.parametrize("M,K,N", [(1024, 1024, 16), (5120, 5120, 16), (5120, 5120, 32), (36880, 8088, 16),
+                                   (36880, 8088, 100), (4101, 1000, 48)])
 def test_graph_capture_replays(torch, usp, M, K, N):
     W, mask, X = wl.make_random(M, K, N, 0.5, seed=M + N)
     A = usp.SparseMatrix(W, mask)
