@@ -344,9 +344,11 @@ template <int NT>
 __device__ inline void compute_tile(lds_u32 *region, const uint8_t *xs, const uint8_t *lut, uint2 msk, int lane,
                                     floatx4 (&acc)[NT]) {
     const StepOffsets so = step_offsets(msk);
-    // Low / high nibble of every mask byte, times 8 (selector table offsets).
-    const uint32_t tlo0 = (msk.x << 3) & 0x78787878u, thi0 = (msk.x >> 1) & 0x78787878u;
-    const uint32_t tlo1 = (msk.y << 3) & 0x78787878u, thi1 = (msk.y >> 1) & 0x78787878u;
+    // Low / high nibble of every mask byte, times 8 (selector table offsets),
+    // opaque to the optimizer so that a step's index is one bit-field extract.
+    uint32_t tlo0 = (msk.x << 3) & 0x78787878u, thi0 = (msk.x >> 1) & 0x78787878u;
+    uint32_t tlo1 = (msk.y << 3) & 0x78787878u, thi1 = (msk.y >> 1) & 0x78787878u;
+    asm("" : "+v"(tlo0), "+v"(thi0), "+v"(tlo1), "+v"(thi1));
     const uint8_t *xb = xs + (lane & 15) * kXRowBytes + 16 * (lane >> 4);
     StepWords cur = read_step(region, lut, so, tlo0, thi0, 0);
 #pragma unroll
@@ -665,8 +667,11 @@ template <int NB>
 __device__ inline void decode_record(lds_u32 *slot, const uint8_t *lut, uint2 msk, const v4u32 (&xb)[NB][kSteps],
                                      floatx4 (&acc)[NB]) {
     const StepOffsets so = step_offsets(msk);
-    const uint32_t tlo0 = (msk.x << 3) & 0x78787878u, thi0 = (msk.x >> 1) & 0x78787878u;
-    const uint32_t tlo1 = (msk.y << 3) & 0x78787878u, thi1 = (msk.y >> 1) & 0x78787878u;
+    uint32_t tlo0 = (msk.x << 3) & 0x78787878u, thi0 = (msk.x >> 1) & 0x78787878u;
+    uint32_t tlo1 = (msk.y << 3) & 0x78787878u, thi1 = (msk.y >> 1) & 0x78787878u;
+    // Opaque to the optimizer: a step's selector index is then one bit-field
+    // extract of these words instead of a shift and a mask of the raw mask.
+    asm("" : "+v"(tlo0), "+v"(thi0), "+v"(tlo1), "+v"(thi1));
     if (NB >= kDecodeAheadMinBlocks) {  // every step's LDS reads first: a short dependency chain per record
         StepWords all[kSteps];
 #pragma unroll
@@ -720,9 +725,14 @@ __global__ __launch_bounds__(W * kLanes) void spmm_chunk_kernel(WaveArgs a, cons
     constexpr int C = kChunkTiles;
     constexpr int kRegion = 1024 * L + 16;  // staged values + the decode's 12-byte overread
     constexpr int kXLoads = NB * 16 * 32 * C / (W * kLanes);  // 16-byte X chunks per thread
-    __shared__ __attribute__((aligned(16))) uint8_t xs[NB * 16 * kChunkXRow];
-    __shared__ __attribute__((aligned(16))) uint8_t regions[W * kRegion];
-    __shared__ __attribute__((aligned(16))) uint8_t lut[16 * 8];
+    // One LDS array: the selector table at its start and the wavefronts'
+    // regions right after it, so that both addresses fit the offset fields of
+    // the decode's LDS reads and cost no instruction per read; the chunk's X
+    // last.
+    __shared__ __attribute__((aligned(16))) uint8_t smem[16 * 8 + W * kRegion + NB * 16 * kChunkXRow];
+    uint8_t *const lut = smem;
+    uint8_t *const regions = smem + 16 * 8;
+    uint8_t *const xs = regions + W * kRegion;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int64_t S = a.maxseg;  // chunks per row block
     const int64_t rg = blockIdx.x / S, seg = blockIdx.x % S;
@@ -1135,8 +1145,11 @@ __global__ __launch_bounds__(64) void densify_kernel(const uint8_t *stream, cons
     for (int c = lane; c < nch; c += kLanes) reinterpret_cast<uint4 *>(region)[c] = vp[c];
     __syncthreads();
     const StepOffsets so = step_offsets(msk);
-    const uint32_t tlo0 = (msk.x << 3) & 0x78787878u, thi0 = (msk.x >> 1) & 0x78787878u;
-    const uint32_t tlo1 = (msk.y << 3) & 0x78787878u, thi1 = (msk.y >> 1) & 0x78787878u;
+    uint32_t tlo0 = (msk.x << 3) & 0x78787878u, thi0 = (msk.x >> 1) & 0x78787878u;
+    uint32_t tlo1 = (msk.y << 3) & 0x78787878u, thi1 = (msk.y >> 1) & 0x78787878u;
+    // Opaque to the optimizer: a step's selector index is then one bit-field
+    // extract of these words instead of a shift and a mask of the raw mask.
+    asm("" : "+v"(tlo0), "+v"(thi0), "+v"(tlo1), "+v"(thi1));
     const int64_t row = rb * kTileRows + (lane & 15);
     if (row >= M) return;
     for (int s = 0; s < kSteps; ++s) {
