@@ -38,9 +38,11 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=100)
-    ap.add_argument("--workload", default="attn13b")
+    # Default: the 70B-class FFN layer (28672 x 8192) at 50% sparsity and 16
+    # tokens, the largest configured layer with the metric's instance.
+    ap.add_argument("--workload", default="ffn70b")
     ap.add_argument("--N", type=int, default=16)
-    ap.add_argument("--sparsity", type=int, default=None)
+    ap.add_argument("--sparsity", type=int, default=50)
     ap.add_argument("--rotate-gib", type=float, default=1.0)
     ap.add_argument("--mode", choices=("graph", "eager"), default="graph")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -48,6 +50,9 @@ def parse():
     ap.add_argument("--no-dense", action="store_true", help="skip the hipBLASLt dense baseline")
     ap.add_argument("--no-tune", action="store_true", help="skip the tuned (best-solution) hipBLASLt baseline")
     ap.add_argument("--no-stream-peak", action="store_true", help="skip the 1 GiB device-copy bandwidth probe")
+    ap.add_argument("--profile", action="store_true",
+                    help="only the warm-up and the timed replay of the sparse product (for rocprofv3 runs: "
+                         "every traced call then streams W from HBM)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run an untimed 256 MiB device copy: the reference kernel that scales "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE readings to bytes")
@@ -59,33 +64,41 @@ def kernel_source_digest() -> str:
 
 
 def timed_steps(torch, step_fns, steps, warmup, mode):
-    """Average ms per step over exactly `steps` steps (after `warmup` eager steps)."""
+    """Average ms per step over exactly `steps` steps (after `warmup` eager steps).
+
+    Step i runs step_fns[i % R]. Right before the timed region one eager pass
+    runs all R functions in the same cyclic order (0 .. R-1), so every timed
+    step's weights were last touched exactly R calls earlier, whatever `steps`
+    is: with R copies spanning >= 1 GiB, each timed call reads its weights from
+    HBM, not from the 256 MB Infinity Cache.
+    """
+    R = len(step_fns)
     for i in range(warmup):
-        step_fns[i % len(step_fns)]()
+        step_fns[i % R]()
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
+    g = None
     if mode == "graph":
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             for i in range(steps):
-                step_fns[i % len(step_fns)]()
+                step_fns[i % R]()
         g.replay()  # first replay uploads the graph; not timed
         torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        g.replay()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / steps
-        del g
-        return ms
+    for i in range(R):  # pre-roll: ends on copy R - 1, the one before the first timed step
+        step_fns[i]()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
-    for i in range(steps):
-        step_fns[i % len(step_fns)]()
+    if g is not None:
+        g.replay()
+    else:
+        for i in range(steps):
+            step_fns[i % R]()
     e1.record(stream)
     torch.cuda.synchronize()
-    return e0.elapsed_time(e1) / steps
+    ms = e0.elapsed_time(e1) / steps
+    del g
+    return ms
 
 
 def per_call_us(torch, step_fns, calls):
@@ -153,6 +166,17 @@ def same_size_read_us(torch, nbytes, reps=200, waves=4096):
     return us
 
 
+def calibration_copies(torch):
+    """Three untimed 256 MiB device copies: the reference kernel whose rocprofv3
+    FETCH_SIZE / WRITE_SIZE readings scale the counters to bytes."""
+    src = torch.empty(256 * 2**20, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    return src.numel()
+
+
 def cpu_baseline(inst, seconds):
     import oracle
     lib = oracle.load()
@@ -178,13 +202,17 @@ def cpu_baseline(inst, seconds):
             "sample": f"{reps} x {rows_n} of {inst.M} output rows (all K={inst.K}, N={inst.N}), {dt:.1f} s, float64"}
 
 
-def traffic_record(kernel_digest):
-    """HBM bytes per launch from committed rocprofv3 counter runs, if they match this kernel source."""
-    path = os.path.join(ROOT, "profiles", "spmm_attn13b_n16_traffic.json")
+def traffic_record(kernel_digest, workload, sparsity, N):
+    """HBM bytes per launch from the committed rocprofv3 counter runs of this
+    exact instance (workload, sparsity, tokens), if they were taken on this
+    kernel source; None otherwise."""
+    path = os.path.join(ROOT, "profiles", f"spmm_{workload}_s{sparsity}_n{N}_traffic.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
     if rec.get("kernel_source_sha256_16") != kernel_digest:
+        return None
+    if (rec.get("workload"), rec.get("sparsity_pct"), rec.get("N")) != (workload, sparsity, N):
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -337,6 +365,16 @@ def main():
     ws = first.make_workspace(N)
     steps = [lambda A=A: usp.usp_spmm(A.handle, X, Y, ws) for A in mats]
     ms = timed_steps(torch, steps, args.steps, args.warmup, args.mode)
+    if args.profile:
+        if args.calibrate_copy:
+            calibration_copies(torch)
+        print(json.dumps({"profile": args.workload, "N": N, "sparsity_pct": inst.sparsity_pct,
+                          "us_per_call": ms * 1e3, "copies": copies,
+                          "algorithmic_bytes_per_step": wbytes + 2 * K * N + 2 * M * N,
+                          "kernel_source_sha256_16": kernel_source_digest()}), flush=True)
+        for A in mats:
+            A.free()
+        return
     p10, p50, p90 = per_call_us(torch, steps, max(200, min(args.steps, 1000)))
     warm_ms = timed_steps(torch, steps[:1], args.steps, 10, args.mode)  # one copy: served from the MALL
 
@@ -396,7 +434,8 @@ def main():
                                f"({inst.prune} magnitude pruning), X {K}x{N} fp16, N={N}",
                    "M": M, "K": K, "N": N, "sparsity_pct": inst.sparsity_pct, "nnz": inst.nnz},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic_record(digest)},
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic_record(digest, args.workload, inst.sparsity_pct, N)},
         "us_per_call": ms * 1e3,
         "us_per_call_p10_p50_p90_eager": [p10, p50, p90],
         "warm_us_per_call": warm_ms * 1e3,
@@ -418,12 +457,7 @@ def main():
         out["same_size_read"] = {"us": rd, "GBps": wbytes / rd / 1e3, "bytes": wbytes,
                                  "frac_of_same_size_read": rd / (ms * 1e3)}  # read time / product time
     if args.calibrate_copy:
-        src = torch.empty(256 * 2**20, dtype=torch.uint8, device="cuda").fill_(1)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        out["calibration_copy_bytes"] = src.numel()
+        out["calibration_copy_bytes"] = calibration_copies(torch)
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(inst, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -55,7 +55,8 @@ typedef enum {
  * with the library). Blocking.
  *   W     host pointer, M x K fp16 bit patterns, row stride ldw >= K
  *   mask  host pointer, M x K bytes, row stride ldm >= K; nonzero = keep
- *   M, K  >= 1
+ *   M, K  >= 1, M <= 2^20 (USP_ERR_UNSUPPORTED above: the workspace keeps one
+ *         arrival counter per 16 rows in a fixed 256 KB region)
  *   device  HIP device ordinal that will hold the encoding
  *   out   receives the new handle; set to NULL on any error
  * Kept values are stored as opaque 16-bit words (signed zeros, subnormals,
@@ -82,8 +83,7 @@ size_t usp_workspace_size(const usp_matrix *A, int64_t N);
  *       bytes (may be NULL when that size is 0); owned by the caller; must not be
  *       used by another in-flight call. It must be zero-filled before its first
  *       use; every completed call leaves it ready for the next one (with any
- *       handle of up to 2^20 rows and any N), so it is cleared once, not per
- *       call. A handle with more rows needs a workspace of its own.
+ *       handle and any N), so it is cleared once, not per call.
  * Accumulation is fp32 in a fixed order: results are bitwise reproducible run
  * to run. The output is rounded to fp16 with round-to-nearest-even.
  * Inputs with X not 16-byte aligned or ldx not a multiple of 8 take a slower
@@ -163,7 +163,11 @@ typedef struct {
 usp_status usp_info(const usp_matrix *A, usp_info_t *info);
 
 /* usp_free -- releases the handle and its device memory. NULL is accepted.
- * The caller guarantees no usp_spmm/usp_densify on it is still in flight. */
+ * The caller guarantees no usp_spmm/usp_densify on it is still in flight.
+ * Handles are looked up among the live ones before use, never dereferenced
+ * blindly: passing a freed handle (or any pointer usp_encode did not return)
+ * to any entry point gives USP_ERR_INVALID_ARG, unless a later usp_encode
+ * happened to return the same address. */
 usp_status usp_free(usp_matrix *A);
 
 /* usp_last_error -- message of the calling thread's most recent failure ("" if none). */

@@ -3,8 +3,10 @@
 #include <hip/hip_runtime.h>
 
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
+#include <unordered_set>
 
 #include "usp_internal.h"
 
@@ -26,7 +28,27 @@ struct DeviceGuard {
     }
 };
 
-bool alive(const usp_matrix *A) { return A && A->magic == usp::kMagic; }
+// Every handle usp_encode returned and usp_free has not released. A handle is
+// checked against this set before it is dereferenced, so a freed (or never
+// issued) pointer is reported instead of read.
+std::mutex g_live_mu;
+std::unordered_set<const usp_matrix *> g_live;
+
+bool alive(const usp_matrix *A) {
+    if (!A) return false;
+    std::lock_guard<std::mutex> lk(g_live_mu);
+    return g_live.count(A) != 0;
+}
+
+// Releases a handle's device memory and the handle itself (registered or not).
+void release(usp_matrix *A) {
+    {
+        DeviceGuard g(A->device);
+        if (A->d_stream) (void)hipFree(A->d_stream);
+        if (A->d_off) (void)hipFree(A->d_off);
+    }
+    delete A;
+}
 
 usp_status hip_fail(hipError_t e, const char *what) {
     return usp::fail(USP_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
@@ -51,6 +73,8 @@ usp_status usp_encode(const uint16_t *W, int64_t ldw, const uint8_t *mask, int64
     if (!out || !W || !mask) return usp::fail(USP_ERR_INVALID_ARG, "usp_encode: null pointer");
     if (M < 1 || K < 1) return usp::fail(USP_ERR_INVALID_ARG, "usp_encode: M and K must be >= 1");
     if (ldw < K || ldm < K) return usp::fail(USP_ERR_INVALID_ARG, "usp_encode: ldw and ldm must be >= K");
+    if (M > usp::kMaxRows)
+        return usp::fail(USP_ERR_UNSUPPORTED, "usp_encode: M above 2^20 rows (the workspace's arrival counters)");
     int ndev = 0;
     hipError_t e = hipGetDeviceCount(&ndev);
     if (e != hipSuccess) return hip_fail(e, "usp_encode: hipGetDeviceCount");
@@ -66,7 +90,6 @@ usp_status usp_encode(const uint16_t *W, int64_t ldw, const uint8_t *mask, int64
     if (!g.ok) return usp::fail(USP_ERR_HIP, "usp_encode: cannot select device");
     usp_matrix *A = new (std::nothrow) usp_matrix();
     if (!A) return usp::fail(USP_ERR_OOM, "usp_encode: host allocation failed");
-    A->magic = usp::kMagic;
     A->device = device;
     A->M = M;
     A->K = K;
@@ -85,15 +108,19 @@ usp_status usp_encode(const uint16_t *W, int64_t ldw, const uint8_t *mask, int64
     if (e == hipSuccess) e = hipMemset(A->d_stream, 0, A->stream_bytes + usp::kStreamPad);
     if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&A->d_off), enc.off.size() * sizeof(uint32_t));
     if (e != hipSuccess) {
-        usp_free(A);
+        release(A);
         return usp::fail(USP_ERR_OOM, std::string("usp_encode: hipMalloc: ") + hipGetErrorString(e));
     }
     e = hipMemcpy(A->d_stream, enc.stream.data(), A->stream_bytes, hipMemcpyHostToDevice);
     if (e == hipSuccess)
         e = hipMemcpy(A->d_off, enc.off.data(), enc.off.size() * sizeof(uint32_t), hipMemcpyHostToDevice);
     if (e != hipSuccess) {
-        usp_free(A);
+        release(A);
         return hip_fail(e, "usp_encode: hipMemcpy");
+    }
+    {
+        std::lock_guard<std::mutex> lk(g_live_mu);
+        g_live.insert(A);
     }
     *out = A;
     return USP_OK;
@@ -217,14 +244,11 @@ usp_status usp_info(const usp_matrix *A, usp_info_t *info) {
 
 usp_status usp_free(usp_matrix *A) {
     if (!A) return USP_OK;
-    if (!alive(A)) return usp::fail(USP_ERR_INVALID_ARG, "usp_free: invalid or already freed handle");
     {
-        DeviceGuard g(A->device);
-        if (A->d_stream) (void)hipFree(A->d_stream);
-        if (A->d_off) (void)hipFree(A->d_off);
+        std::lock_guard<std::mutex> lk(g_live_mu);
+        if (g_live.erase(A) == 0) return usp::fail(USP_ERR_INVALID_ARG, "usp_free: invalid or already freed handle");
     }
-    A->magic = 0;
-    delete A;
+    release(A);
     return USP_OK;
 }
 

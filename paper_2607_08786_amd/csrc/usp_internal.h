@@ -10,7 +10,6 @@
 #include "usp_format.h"
 
 struct usp_matrix {
-    uint32_t magic;          // kMagic while alive
     int device;
     int64_t M, K;            // logical shape
     int64_t RB, KT;          // row blocks (16 rows) and column tiles (256 columns)
@@ -24,7 +23,10 @@ struct usp_matrix {
 
 namespace usp {
 
-constexpr uint32_t kMagic = 0x55535031u;  // "USP1"
+// Most rows an encoding may have: the workspace's arrival counters (one
+// 32-bit word per row block, rounded up to sets of 4) occupy a fixed 256 KB
+// region at its start whatever the handle.
+constexpr int64_t kMaxRows = int64_t(1) << 20;
 
 // Host-side encoding result (before upload).
 struct HostEncoding {
@@ -65,5 +67,4 @@ struct Epilogue {
 int launch_spmm(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy, int64_t N,
                 const Epilogue &ep, void *workspace, void *stream);
 int launch_densify(const usp_matrix *A, void *Wd, int64_t ldw, void *stream);
-
 }  // namespace usp

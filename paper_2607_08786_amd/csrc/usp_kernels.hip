@@ -58,7 +58,6 @@ constexpr int kGroupRows = kWaves * kTileRows;         // rows of a row group (6
 constexpr int kWRegionBytes = kMaxValBytes;            // 8 KB per wavefront (8 KB aligned)
 constexpr int kXRowBytes = kTileK * 2 + 16;            // 528: padded token row of the X tile
 constexpr int kMaxNT = 8;                              // 16-token blocks per pass (N <= 128)
-constexpr int kWgsPerCu = 3;                           // persistent workgroups per CU
 
 struct SpmmArgs {
     const uint8_t *stream;
@@ -1412,8 +1411,11 @@ static WaveKind wave_kind(const usp_matrix *A, int loads, int64_t N) {
     // (224 row blocks x 32 tiles) takes 16.8 us on it at 16 tokens against 14.8
     // on the column-chunk kernel, but 13.6 against 14.5 at 8 tokens; the tiny
     // layer (4 tiles) 4.5 against 6.6.
+    // A wavefront of the row-block kernel reads its stretch of the offset table
+    // (up to ceil(KT / 2) tiles at its fewest 2 wavefronts, plus one end entry)
+    // with one 64-lane load, so the stretch is limited to 63 tiles.
     if (nb == 1 && A->RB * A->KT <= kSmallMaxTiles && A->RB <= (A->num_cus > 0 ? A->num_cus : 256) &&
-        (A->KT <= kRowMaxTiles || N <= 8))
+        (A->KT <= kRowMaxTiles || N <= 8) && ceil_div(A->KT, 2) <= kLanes - 1)
         return kWaveRow;
     if (nb <= kMaxChunkTokenBlocks && A->RB * A->KT <= kChunkMaxTiles && ceil_div(A->KT, kChunkTiles) <= kChunkMaxSplit) {
         if (nb == 1) return kWaveChunk;
@@ -1515,20 +1517,18 @@ std::string describe_plan(const usp_matrix *A, int64_t N) {
     return buf;
 }
 
-// Workspace: one uint32 arrival counter per row group at offset 0 (shared by
-// every pass, zero between passes), padded to 256 bytes, then the fp32 partials
-// of the current pass [row group][slot][tokens][64 rows].
+// Workspace: the arrival counters at offset 0 (zero between calls), then the
+// fp32 partials of the current pass.
 // The counters take the first kCounterRegionBytes of every workspace whatever
-// the handle (one per row block, rounded up to whole sets of 4, fits for up to
-// 2^20 rows; also one per row group and one per row set and token group), and
-// the partials start after it: partials a call leaves behind never sit where
-// another handle's counters are, so one zero-filled workspace serves calls with
-// any handle and any N. Larger handles need a workspace of their own.
+// the handle (one word per row block, rounded up to whole sets of 4, for up to
+// kMaxRows rows, which usp_encode enforces; the four-wavefront kernel's one per
+// row group and the direct-to-LDS kernel's one per row set and token group fit
+// the same region), and the partials start after it: partials a call leaves
+// behind never sit where another handle's counters are, so one zero-filled
+// workspace serves calls with any handle and any N.
 constexpr size_t kCounterRegionBytes = 256 * 1024;
-static size_t counters_bytes(const usp_matrix *A) {
-    const size_t need = ((size_t)ceil_div(A->RB, kDmaRows) * kDmaRows * sizeof(uint32_t) + 255) / 256 * 256;
-    return need > kCounterRegionBytes ? need : kCounterRegionBytes;
-}
+static_assert(kMaxRows / kTileRows * sizeof(uint32_t) <= kCounterRegionBytes, "counter region too small");
+static size_t counters_bytes(const usp_matrix *) { return kCounterRegionBytes; }
 
 static size_t partials_bytes(const SpmmPlan &p, int64_t nb) {
     return (size_t)p.row_groups * (size_t)p.maxseg * (size_t)nb * kGroupRows * sizeof(float);

@@ -88,6 +88,16 @@ def _check(status: int):
         raise UspError(status, usp_last_error())
 
 
+def _torch_stream(stream):
+    """The torch stream a call is enqueued on: the current one, a torch.cuda.Stream, or a raw
+    hipStream_t handle wrapped as an external stream."""
+    if stream is None:
+        return torch.cuda.current_stream()
+    if isinstance(stream, torch.cuda.Stream):
+        return stream
+    return torch.cuda.ExternalStream(int(stream))
+
+
 def _stream_handle(stream) -> int | None:
     if stream is None:
         return torch.cuda.current_stream().cuda_stream
@@ -214,21 +224,29 @@ class SparseMatrix:
     def plan(self, N: int) -> str:
         return usp_plan(self.handle, N)
 
-    def make_workspace(self, N: int) -> torch.Tensor | None:
+    def make_workspace(self, N: int, stream=None) -> torch.Tensor | None:
+        """A zero-filled workspace for N tokens, allocated and cleared on `stream` (default: the
+        current stream), so calls enqueued on that stream are ordered after the clear."""
         n = self.workspace_size(N)
         if n == 0:
             return None
-        return torch.zeros(n, dtype=torch.uint8, device=f"cuda:{self.device}")  # zeroed once
+        with torch.cuda.stream(_torch_stream(stream)):
+            return torch.zeros(n, dtype=torch.uint8, device=f"cuda:{self.device}")  # zeroed once
 
     def spmm(self, X: torch.Tensor, Y: torch.Tensor | None = None, workspace=None, stream=None,
              bias: torch.Tensor | None = None, residual: torch.Tensor | None = None,
              activation: str | int = "none") -> torch.Tensor:
-        """Y = W X (token-major), or act(W X + bias) + residual when any of those is given."""
+        """Y = W X (token-major), or act(W X + bias) + residual when any of those is given.
+
+        A Y or workspace this call creates is allocated on `stream`, the stream the product is
+        enqueued on, so the caching allocator only reuses that memory in that stream's order."""
         N = X.shape[0]
-        if Y is None:
-            Y = torch.empty((N, self.M), dtype=torch.float16, device=X.device)
-        if workspace is None:
-            workspace = self.make_workspace(N)
+        if Y is None or workspace is None:
+            with torch.cuda.stream(_torch_stream(stream)):
+                if Y is None:
+                    Y = torch.empty((N, self.M), dtype=torch.float16, device=X.device)
+                if workspace is None:
+                    workspace = self.make_workspace(N)
         if bias is None and residual is None and activation in ("none", 0):
             usp_spmm(self.handle, X, Y, workspace, stream)
         else:

@@ -56,6 +56,22 @@ def test_argument_errors_without_device(usp):
     assert "ldw" in usp.usp_last_error()
     assert lib.usp_densify(None, None, 0, None) == 1
     assert lib.usp_decode(None, None, None) == 1
+    # More than 2^20 rows: refused before W or the mask is read.
+    assert lib.usp_encode(buf, 4, mb, 4, (1 << 20) + 1, 4, 0, ctypes.byref(h)) == 2
+    assert "2^20" in usp.usp_last_error() and h.value is None
+
+
+def test_unknown_handles_are_rejected_without_being_read(usp):
+    """A pointer usp_encode never returned (here: ordinary host memory holding
+    garbage) is looked up, not dereferenced: every entry point says invalid."""
+    lib = usp.load_library()
+    junk = ctypes.create_string_buffer(b"\xff" * 512)
+    fake = ctypes.cast(junk, ctypes.c_void_p)
+    info = usp.usp_info_t()
+    assert lib.usp_info(fake, ctypes.byref(info)) == 1
+    assert lib.usp_workspace_size(fake, 16) == 0
+    assert lib.usp_spmm(fake, fake, 8, fake, 8, 16, None, 0, None) == 1
+    assert lib.usp_free(fake) == 1 and "freed" in usp.usp_last_error()
 
 
 def test_last_error_is_thread_local(usp):

@@ -668,7 +668,7 @@ def test_concurrent_host_threads(torch, usp):
     def work(A, Xd, ref):
         try:
             st = torch.cuda.Stream()
-            ws = A.make_workspace(Xd.shape[0])
+            ws = A.make_workspace(Xd.shape[0], stream=st)  # zeroed on st, before the products
             with torch.cuda.stream(st):
                 for _ in range(10):
                     Y = A.spmm(Xd, workspace=ws)
@@ -686,3 +686,37 @@ def test_concurrent_host_threads(torch, usp):
     for A, _, _ in cases:
         A.free()
     assert not errors, errors
+
+
+# Long row blocks with few tokens: the row-block kernel serves them only while a
+# wavefront's stretch of the offset table fits one 64-lane load (at most 126
+# column tiles); 16 x 140000 at 4 tokens (547 column tiles) goes to another
+# kernel. Exact on small integers, every output.
+@pytest.mark.parametrize("M,K,N,route", [(16, 32256, 4, "row"), (16, 140000, 4, "fourwave"), (40, 90000, 8, "fourwave")])
+def test_long_row_blocks_exact(torch, usp, M, K, N, route):
+    W, mask, X = wl.make_small_int(M, K, N, 0.5, seed=K + N, lo=-1, hi=1)
+    A = usp.SparseMatrix(W, mask)
+    plan = A.plan(N)
+    print(f"case M={M} K={K} N={N}: {plan}", flush=True)
+    A.free()
+    assert plan.startswith(route), plan
+    Y = run(torch, usp, W, mask, X)
+    Yref, _ = oracle.masked_gemm(W, mask, X)
+    assert np.array_equal(Y, Yref)
+
+
+# Handle lifetime: a freed handle is rejected by every entry point (it is looked
+# up among the live handles, never dereferenced), and a second free is an error.
+def test_freed_handle_rejected(torch, usp):
+    W, mask, X = wl.make_random(64, 512, 16, 0.5, seed=8)
+    A = usp.SparseMatrix(W, mask)
+    h = A.handle
+    usp.usp_free(h)
+    A.handle = None
+    lib = usp.load_library()
+    Xd = to_dev(torch, X)
+    Y = torch.empty((16, 64), dtype=torch.float16, device="cuda")
+    assert lib.usp_spmm(h, Xd.data_ptr(), 512, Y.data_ptr(), 64, 16, None, 0, None) == 1
+    assert "freed" in usp.usp_last_error()
+    assert lib.usp_free(h) == 1
+    assert lib.usp_workspace_size(h, 16) == 0

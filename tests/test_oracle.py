@@ -56,16 +56,3 @@ def test_activations_pinned():
         assert abs(d0 - 0.5) < 1e-6
         slope = np.diff(oracle.activation(x, a)) / np.diff(x)
         assert slope.max() < oracle.ACT_SLOPE_BOUND and slope.max() > 1.05
-
-
-def test_linear_epilogue_scale():
-    import numpy as np
-    rng = np.random.default_rng(4)
-    Y = rng.normal(size=(3, 5)); A = np.abs(Y) + 1.0
-    b = rng.normal(size=5); r = rng.normal(size=(3, 5))
-    y0, s0 = oracle.linear_epilogue(Y, A, 0)
-    assert np.array_equal(y0, Y) and np.array_equal(s0, A)
-    y1, s1 = oracle.linear_epilogue(Y, A, 1, bias=b, residual=r)
-    assert np.allclose(y1, np.maximum(Y + b, 0) + r) and np.allclose(s1, A + np.abs(b) + np.abs(r))
-    _, s3 = oracle.linear_epilogue(Y, A, 3, bias=b)
-    assert np.allclose(s3, oracle.ACT_SLOPE_BOUND * (A + np.abs(b)))
