@@ -125,6 +125,30 @@ usp_status usp_spmm_ex(const usp_matrix *A, const void *X, int64_t ldx, void *Y,
                        const void *bias, const void *residual, int64_t ldr, int activation,
                        void *workspace, size_t ws_bytes, void *stream);
 
+/* Bytes of the device scratch usp_spmm_noalloc uses on each GPU (32 MiB). */
+#define USP_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+/*
+ * usp_spmm_noalloc -- for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc. The same product as usp_spmm (same kernels, same bits), with no
+ * workspace argument: its workspace is a USP_NOALLOC_SCRATCH_BYTES device array
+ * the library holds on each GPU until the process ends (looked up and cleared
+ * once per device inside usp_encode, so the handle's device is set up by the
+ * time any product runs). This call allocates nothing and calls no allocating
+ * routine.
+ *   A, X, ldx, Y, ldy, N, stream   as usp_spmm
+ * Every call on a GPU shares that GPU's scratch, which keeps the last call's
+ * contents; each completed call leaves its arrival counters at zero, as the
+ * next call needs them. Calls that overlap in time on one GPU (other streams,
+ * other host threads) race on the scratch and give wrong results: serialize
+ * them. Returns USP_ERR_UNSUPPORTED, enqueueing nothing, when the product needs
+ * more workspace than the scratch holds (usp_workspace_size(A, N) >
+ * USP_NOALLOC_SCRATCH_BYTES; every configured layer up to 64 tokens fits).
+ */
+usp_status usp_spmm_noalloc(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy,
+                            int64_t N, void *stream);
+
 /*
  * usp_plan -- which kernel usp_spmm runs for this handle and N when X is 16-byte
  * aligned with ldx = K, as a short text ("row W=8", "chunk S=5 W=8 nb=1 grid=200",

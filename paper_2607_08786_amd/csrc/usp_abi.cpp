@@ -111,6 +111,13 @@ usp_status usp_encode(const uint16_t *W, int64_t ldw, const uint8_t *mask, int64
         release(A);
         return usp::fail(USP_ERR_OOM, std::string("usp_encode: hipMalloc: ") + hipGetErrorString(e));
     }
+    // One-time set-up of this device's scratch for usp_spmm_noalloc (outside
+    // any graph capture: encoding precedes every product).
+    if (e == hipSuccess) e = (hipError_t)usp::noalloc_setup(device);
+    if (e != hipSuccess) {
+        release(A);
+        return hip_fail(e, "usp_encode: device scratch set-up");
+    }
     e = hipMemcpy(A->d_stream, enc.stream.data(), A->stream_bytes, hipMemcpyHostToDevice);
     if (e == hipSuccess)
         e = hipMemcpy(A->d_off, enc.off.data(), enc.off.size() * sizeof(uint32_t), hipMemcpyHostToDevice);
@@ -186,6 +193,22 @@ usp_status usp_spmm_ex(const usp_matrix *A, const void *X, int64_t ldx, void *Y,
     ep.ldr = ldr;
     ep.act = activation;
     return spmm_common("usp_spmm_ex", A, X, ldx, Y, ldy, N, ep, workspace, ws_bytes, stream);
+}
+
+usp_status usp_spmm_noalloc(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy, int64_t N,
+                            void *stream) {
+    if (!alive(A)) return usp::fail(USP_ERR_INVALID_ARG, "usp_spmm_noalloc: invalid or freed handle");
+    if (N < 1) return usp::fail(USP_ERR_INVALID_ARG, "usp_spmm_noalloc: N must be >= 1");
+    const size_t need = usp::spmm_workspace_bytes(A, N);
+    if (need > USP_NOALLOC_SCRATCH_BYTES)
+        return usp::fail(USP_ERR_UNSUPPORTED, "usp_spmm_noalloc: this product needs " + std::to_string(need) +
+                                                  " bytes of workspace, above the " +
+                                                  std::to_string((size_t)USP_NOALLOC_SCRATCH_BYTES) +
+                                                  "-byte device scratch (use usp_spmm with a workspace)");
+    void *ws = usp::noalloc_scratch(A->device);
+    if (!ws) return usp::fail(USP_ERR_INTERNAL, "usp_spmm_noalloc: device scratch not set up");
+    return spmm_common("usp_spmm_noalloc", A, X, ldx, Y, ldy, N, usp::Epilogue(), ws, USP_NOALLOC_SCRATCH_BYTES,
+                       stream);
 }
 
 usp_status usp_densify(const usp_matrix *A, void *Wd, int64_t ldw, void *stream) {

@@ -67,4 +67,10 @@ struct Epilogue {
 int launch_spmm(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_t ldy, int64_t N,
                 const Epilogue &ep, void *workspace, void *stream);
 int launch_densify(const usp_matrix *A, void *Wd, int64_t ldw, void *stream);
+// Device scratch of usp_spmm_noalloc: noalloc_setup looks up and clears the
+// calling thread's current device's copy once (returns a HIP error code);
+// noalloc_scratch returns its device address, or null before the set-up.
+int noalloc_setup(int device);
+void *noalloc_scratch(int device);
+
 }  // namespace usp

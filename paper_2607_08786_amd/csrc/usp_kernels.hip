@@ -36,6 +36,7 @@
 #include <algorithm>
 #include <atomic>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "usp_internal.h"
@@ -1667,6 +1668,41 @@ int launch_spmm(const usp_matrix *A, const void *X, int64_t ldx, void *Y, int64_
         if (e != hipSuccess) return (int)e;
     }
     return 0;
+}
+
+// ---------------------------------------------------------------------------
+// Device scratch of usp_spmm_noalloc: the workspace (arrival counters, then
+// partials) of callers that cannot allocate. One copy per GPU, held until the
+// process ends. In host code `scratch` names a host-side stand-in, not device
+// memory: its device address on each GPU is looked up once (with that GPU
+// current) and only that address is used.
+// ---------------------------------------------------------------------------
+
+static __device__ __align__(256) uint8_t scratch[USP_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+static std::atomic<void *> g_scratch[kMaxDevices];
+static std::mutex g_scratch_mu;
+
+int noalloc_setup(int device) {
+    if (device < 0 || device >= kMaxDevices) return (int)hipErrorInvalidDevice;
+    if (g_scratch[device].load(std::memory_order_acquire)) return 0;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (g_scratch[device].load(std::memory_order_relaxed)) return 0;
+    void *ptr = nullptr;  // the caller made `device` current
+    hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return (int)e;
+    // The arrival counters must start at zero; every completed product leaves
+    // them at zero again.
+    e = hipMemsetAsync(ptr, 0, kCounterRegionBytes, nullptr);
+    if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
+    if (e != hipSuccess) return (int)e;
+    g_scratch[device].store(ptr, std::memory_order_release);
+    return 0;
+}
+
+void *noalloc_scratch(int device) {
+    return device >= 0 && device < kMaxDevices ? g_scratch[device].load(std::memory_order_acquire) : nullptr;
 }
 
 int launch_densify(const usp_matrix *A, void *Wd, int64_t ldw, void *stream) {

@@ -20,8 +20,11 @@ USP_OK = 0
 _STATUS = {0: "USP_OK", 1: "USP_ERR_INVALID_ARG", 2: "USP_ERR_UNSUPPORTED", 3: "USP_ERR_OOM",
            4: "USP_ERR_HIP", 5: "USP_ERR_INTERNAL"}
 
-EXPORTED = ("usp_encode", "usp_workspace_size", "usp_spmm", "usp_spmm_ex", "usp_plan", "usp_densify",
-            "usp_decode", "usp_info", "usp_free", "usp_last_error")
+EXPORTED = ("usp_encode", "usp_workspace_size", "usp_spmm", "usp_spmm_ex", "usp_spmm_noalloc", "usp_plan",
+            "usp_densify", "usp_decode", "usp_info", "usp_free", "usp_last_error")
+
+# Bytes of the per-GPU device scratch usp_spmm_noalloc uses (USP_NOALLOC_SCRATCH_BYTES).
+NOALLOC_SCRATCH_BYTES = 32 << 20
 
 # usp_activation
 ACTIVATIONS = {"none": 0, "relu": 1, "gelu_tanh": 2, "silu": 3}
@@ -62,6 +65,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.usp_spmm.restype = st
     lib.usp_spmm_ex.argtypes = [p, p, i64, p, i64, i64, p, p, i64, ctypes.c_int, p, sz, p]
     lib.usp_spmm_ex.restype = st
+    lib.usp_spmm_noalloc.argtypes = [p, p, i64, p, i64, i64, p]
+    lib.usp_spmm_noalloc.restype = st
     lib.usp_plan.argtypes = [p, i64, ctypes.c_char_p, sz]
     lib.usp_plan.restype = st
     lib.usp_densify.argtypes = [p, p, i64, p]
@@ -181,6 +186,20 @@ def usp_spmm_ex(handle: int, X: torch.Tensor, Y: torch.Tensor, workspace: torch.
         ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
     _check(load_library().usp_spmm_ex(handle, X.data_ptr(), X.stride(0), Y.data_ptr(), Y.stride(0), N,
                                       b_ptr, r_ptr, ldr, act, ws_ptr, ws_bytes, _stream_handle(stream)))
+
+
+def usp_spmm_noalloc(handle: int, X: torch.Tensor, Y: torch.Tensor, stream=None) -> None:
+    """usp_spmm with the library's per-GPU device scratch as its workspace (no allocation;
+    calls overlapping on one GPU must be serialized by the caller)."""
+    if X.dtype != torch.float16 or Y.dtype != torch.float16:
+        raise TypeError("X and Y must be float16")
+    if X.dim() != 2 or Y.dim() != 2 or X.stride(1) != 1 or Y.stride(1) != 1:
+        raise TypeError("X and Y must be 2-D with unit inner stride")
+    N = X.shape[0]
+    if Y.shape[0] != N:
+        raise ValueError("X and Y must have the same number of tokens")
+    _check(load_library().usp_spmm_noalloc(handle, X.data_ptr(), X.stride(0), Y.data_ptr(), Y.stride(0), N,
+                                           _stream_handle(stream)))
 
 
 def usp_densify(handle: int, Wd: torch.Tensor, stream=None) -> None:
