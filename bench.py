@@ -166,6 +166,69 @@ def same_size_read_us(torch, nbytes, reps=200, waves=4096):
     return us
 
 
+def hipblaslt_best(torch, M, K, N, Wds, X, steps, warmup, max_algos=16):
+    """Dense baseline through hipBLASLt's C API (libusp_denseref.so): fp16 A/B/C,
+    fp32 compute, TN layout. Every algorithm of the heuristic's top `max_algos` is
+    timed over the same cold rotation of weight copies (eager back-to-back calls);
+    the best is timed again as a graph replay and the faster of the two kept."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2607_08786_amd", "libusp_denseref.so"))
+    vp, i64, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t
+    lib.usp_dense_plan.argtypes = [i64, i64, i64, ctypes.c_int, sz, ctypes.POINTER(vp), ctypes.POINTER(ctypes.c_int)]
+    lib.usp_dense_workspace.argtypes = [vp, ctypes.c_int]
+    lib.usp_dense_workspace.restype = sz
+    lib.usp_dense_algo_info.argtypes = [vp, ctypes.c_int, ctypes.c_char_p, sz]
+    lib.usp_dense_run.argtypes = [vp, ctypes.c_int, vp, vp, vp, vp, sz, vp]
+    lib.usp_dense_free.argtypes = [vp]
+    ctx, n = vp(), ctypes.c_int(0)
+    ws_limit = 128 << 20
+    rc = lib.usp_dense_plan(M, K, N, max_algos, ws_limit, ctypes.byref(ctx), ctypes.byref(n))
+    if rc != 0:
+        return {"error": f"usp_dense_plan returned {rc}"}
+    ws = torch.empty(max(1, max(lib.usp_dense_workspace(ctx, i) for i in range(n.value))), dtype=torch.uint8,
+                     device="cuda")
+    Yd = torch.empty((N, M), dtype=torch.float16, device="cuda")
+    st = torch.cuda.current_stream().cuda_stream
+
+    def fns(i):
+        def run(Wx):
+            rc = lib.usp_dense_run(ctx, i, Wx.data_ptr(), X.data_ptr(), Yd.data_ptr(), ws.data_ptr(), ws.numel(), st)
+            if rc != 0:
+                raise RuntimeError(f"hipblasLtMatmul returned {rc}")
+        return [lambda Wx=Wx: run(Wx) for Wx in Wds]
+
+    results = []
+    for i in range(n.value):
+        try:
+            results.append((timed_steps(torch, fns(i), steps, warmup, "eager"), i))
+        except RuntimeError:
+            continue
+    if not results:
+        lib.usp_dense_free(ctx)
+        return {"error": "no hipBLASLt algorithm ran"}
+    results.sort()
+    best_ms, best = results[0]
+    graph_ms = None
+    try:
+        graph_ms = timed_steps(torch, fns(best), steps, warmup, "graph")
+    except Exception:  # capture not supported by this algorithm: the eager time stands
+        pass
+    fns(best)[0]()
+    ref = torch.matmul(X, Wds[0].t())
+    torch.cuda.synchronize()
+    rel = float((Yd.float() - ref.float()).norm() / ref.float().norm().clamp_min(1e-30))
+    name = ctypes.create_string_buffer(256)
+    index = lib.usp_dense_algo_info(ctx, best, name, 256)
+    out = {"ms_per_call": min(best_ms, graph_ms) if graph_ms else best_ms, "eager_ms_per_call": best_ms,
+           "graph_ms_per_call": graph_ms, "algorithm_rank": best, "solution_index": index,
+           "solution_name": name.value.decode(errors="replace"), "algorithms_timed": len(results),
+           "rel_frobenius_vs_torch_matmul": rel,
+           "library": "hipBLASLt C API (hipblasLtMatmul), fp16 A/B/C, fp32 compute, TN layout, best of the "
+                      f"heuristic's top {max_algos}"}
+    lib.usp_dense_free(ctx)
+    return out
+
+
 def calibration_copies(torch):
     """Three untimed 256 MiB device copies: the reference kernel whose rocprofv3
     FETCH_SIZE / WRITE_SIZE readings scale the counters to bytes."""
@@ -391,9 +454,11 @@ def main():
         Yd = torch.empty((N, M), dtype=torch.float16, device="cuda")
         dsteps = [lambda Wx=Wx: torch.matmul(X, Wx.t(), out=Yd) for Wx in Wds]
         dms = timed_steps(torch, dsteps, args.steps, args.warmup, args.mode)
-        dense = {"ms_per_call": dms, "tflops": 2.0 * M * K * N / (dms * 1e-3) / 1e12,
-                 "library": "hipBLASLt via torch.matmul, default heuristic (fp16 in/out, fp32 accumulate)",
-                 "copies": dcopies}
+        dense = {"ms_per_call": dms, "copies": dcopies,
+                 "torch_matmul_ms_per_call": dms,
+                 "torch_matmul_library": "hipBLASLt via torch.matmul, default heuristic (fp16 in/out, fp32 accumulate)"}
+        capi = hipblaslt_best(torch, M, K, N, Wds, X, args.steps, args.warmup)
+        dense["c_api"] = capi
         if not args.no_tune:
             # Best of hipBLASLt's solutions for this shape (PyTorch TunableOp times each).
             import torch.cuda.tunable as tunable
@@ -407,11 +472,16 @@ def main():
                 tms = timed_steps(torch, dsteps, args.steps, args.warmup, args.mode)
                 dense["tuned_ms_per_call"] = tms
                 dense["tuned_library"] = "hipBLASLt, best solution for the shape (PyTorch TunableOp)"
-                dense["best_ms_per_call"] = min(dms, tms)
             except Exception as exc:  # the default-heuristic number stands alone
                 dense["tuned_error"] = repr(exc)[:200]
             finally:
                 tunable.enable(False)
+        # The baseline is the fastest of the three ways of calling hipBLASLt.
+        cands = [("c_api", capi.get("ms_per_call")), ("torch_matmul", dms), ("tunableop", dense.get("tuned_ms_per_call"))]
+        cands = [(v, k) for k, v in cands if v]
+        dense["best_ms_per_call"], dense["best_from"] = min(cands)
+        dense["ms_per_call"] = dense["best_ms_per_call"]
+        dense["tflops"] = 2.0 * M * K * N / (dense["ms_per_call"] * 1e-3) / 1e12
         del Wds
 
     alg_bytes = wbytes + 2 * K * N + 2 * M * N
@@ -448,7 +518,7 @@ def main():
     }
     if dense is not None:
         out["dense_hipblaslt"] = dense
-        out["speedup_vs_hipblaslt"] = dense.get("best_ms_per_call", dense["ms_per_call"]) / ms
+        out["speedup_vs_hipblaslt"] = dense["best_ms_per_call"] / ms
     if not args.no_stream_peak:
         peak = stream_copy_gbps(torch)
         out["stream_copy_GBps"] = peak

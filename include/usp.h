@@ -47,7 +47,7 @@ typedef enum {
 } usp_status;
 
 /* Format version written by usp_encode and reported by usp_info. */
-#define USP_FORMAT_VERSION 1
+#define USP_FORMAT_VERSION 2
 
 /*
  * usp_encode -- one-time conversion of W and its keep-mask into the compressed

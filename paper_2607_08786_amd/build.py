@@ -29,6 +29,7 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError("hipcc failed building libusp.so")
     os.replace(tmp, LIB)
     build_probe(verbose)
+    build_dense_ref(verbose)
     return LIB
 
 
@@ -48,6 +49,24 @@ def build_probe(verbose: bool = False) -> str:
         raise RuntimeError("hipcc failed building libusp_probe.so")
     os.replace(tmp, PROBE_LIB)
     return PROBE_LIB
+
+
+DENSE_LIB = os.path.join(HERE, "libusp_denseref.so")
+
+
+def build_dense_ref(verbose: bool = False) -> str:
+    """libusp_denseref.so: the hipBLASLt dense GEMM the benchmark compares against."""
+    tmp = DENSE_LIB + ".tmp"
+    cmd = [HIPCC, *DEVICE_FLAGS, "-O2", "-std=c++17", "-fPIC", "-shared", "-Wall",
+           os.path.join(CSRC, "usp_dense_ref.cpp"), "-o", tmp, "-lhipblaslt"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        sys.stderr.write(res.stdout + res.stderr)
+        raise RuntimeError("hipcc failed building libusp_denseref.so")
+    os.replace(tmp, DENSE_LIB)
+    return DENSE_LIB
 
 
 if __name__ == "__main__":

@@ -92,12 +92,19 @@ void encode_host(const uint16_t *W, int64_t ldw, const uint8_t *mask, int64_t ld
             for (int s = 0; s < kSteps; ++s) {
                 for (int l = 0; l < kLanes; ++l) {
                     const int r = l % kTileRows, g = l / kTileRows;
-                    const int64_t row = rb * kTileRows + r;
-                    const int64_t col0 = kt * kTileK + tile_col(g, s, 0);
-                    uint8_t b = lane_step_bits(mask, ldm, M, K, row, col0);
-                    rec[8 * l + s] = b;
-                    for (int j = 0; j < 8; ++j)
-                        if (b & (1u << j)) vals[v++] = W[row * ldw + col0 + j];
+                    rec[8 * l + s] = lane_step_bits(mask, ldm, M, K, rb * kTileRows + r, kt * kTileK + tile_col(g, s, 0));
+                }
+                // Values of step s: block (s, low nibble), then block (s, high nibble);
+                // within a block lane 0's values first, in column order.
+                for (int h = 0; h < 2; ++h) {
+                    for (int l = 0; l < kLanes; ++l) {
+                        const uint8_t b = rec[8 * l + s];
+                        const int r = l % kTileRows, g = l / kTileRows;
+                        const int64_t row = rb * kTileRows + r;
+                        const int64_t col0 = kt * kTileK + tile_col(g, s, 0);
+                        for (int j = 4 * h; j < 4 * h + 4; ++j)
+                            if (b & (1u << j)) vals[v++] = W[row * ldw + col0 + j];
+                    }
                 }
             }
         }
@@ -119,12 +126,13 @@ bool decode_host(const HostEncoding &enc, uint16_t *W_out, uint8_t *mask_out) {
             const int64_t cap = ((int64_t)enc.off[t + 1] - enc.off[t] - kMaskChunks) * 8;  // halfs
             const uint16_t *vals = reinterpret_cast<const uint16_t *>(rec + kMaskBytes);
             int64_t v = 0;
-            for (int s = 0; s < kSteps && ok; ++s) {
+            for (int sh = 0; sh < 2 * kSteps && ok; ++sh) {
+                const int s = sh / 2, h = sh % 2;  // block (step s, nibble half h)
                 for (int l = 0; l < kLanes; ++l) {
                     const int r = l % kTileRows, g = l / kTileRows;
                     const int64_t row = rb * kTileRows + r;
                     const uint8_t b = rec[8 * l + s];
-                    for (int j = 0; j < 8; ++j) {
+                    for (int j = 4 * h; j < 4 * h + 4; ++j) {
                         if (!(b & (1u << j))) continue;
                         const int64_t col = kt * kTileK + tile_col(g, s, j);
                         if (row >= M || col >= K || v >= cap) { ok = false; break; }

@@ -1,4 +1,4 @@
-// usp_format.h -- geometry of the compressed weight format (version 1).
+// usp_format.h -- geometry of the compressed weight format (version 2).
 //
 // The paper stores a pruned weight matrix in three layers (Section 3.2): a 2:4
 // part for sparse tensor cores, a slot-filling part with differential position
@@ -19,11 +19,14 @@
 // Tile record (starts on a 16-byte boundary, byte offset 16 * off[t]):
 //   [0, 512)            mask: lane l's 8 bytes at 8 l; byte s bit j = position
 //                       (s, j) above is kept.
-//   [512, 512 + 2 nnz)  kept values as fp16 bit patterns, step-major: all of
-//                       step 0's values (lane 0's, j ascending, then lane 1's, ...,
-//                       then lane 63's), then step 1's, ..., then step 7's.
-//                       At any step the 64 lanes read neighbouring words, which
-//                       keeps the on-chip gather free of LDS bank conflicts.
+//   [512, 512 + 2 nnz)  kept values as fp16 bit patterns in 16 blocks, block
+//                       b = 2 s + h holding nibble h of step s (h = 0: positions
+//                       j = 0..3, h = 1: j = 4..7) of every lane: lane 0's kept
+//                       values of that nibble (j ascending), then lane 1's, ...,
+//                       then lane 63's; blocks in order b = 0..15, unpadded.
+//                       A lane's nibble has 0-4 values, so the 64 lanes reading
+//                       their nibble of one block read words about one dword
+//                       apart (32 lanes span about the 32 LDS banks).
 //   zero padding to a multiple of 16 bytes.
 // off[] holds T + 1 uint32 entries in 16-byte units; off[T] is the total size.
 #pragma once

@@ -133,12 +133,15 @@ __device__ inline lds_u32 *as_lds(const void *p) {
     return (lds_u32 *)(const __attribute__((address_space(3))) void *)p;
 }
 
-// region: the staged values. The byte offset is bounded by the largest record
-// (8 KB), so a read never leaves the region's neighbourhood.
+// region: the staged values. hb is the nibble's first byte (even); the three
+// dwords from its dword hold its up to 4 values whatever its alignment. A read
+// may run up to 12 bytes past the record's values, which every region leaves
+// room for.
 __device__ inline void read_nibble(lds_u32 *region, uint32_t hb, uint32_t idx8, const uint8_t *lut,
                                    uint32_t *e, uint2 &sel) {
     typedef const __attribute__((address_space(3))) uint8_t lds_u8;
-    lds_u32 *d = (lds_u32 *)((lds_u8 *)region + (hb & (kWRegionBytes - 4)));
+    typedef volatile const __attribute__((address_space(3))) uint32_t lds_vu32;
+    lds_vu32 *d = (lds_vu32 *)((lds_u8 *)region + (hb & ~3u));
     e[0] = d[0];
     e[1] = d[1];
     e[2] = d[2];
@@ -156,7 +159,7 @@ __device__ inline void finish_nibble(const uint32_t *e, uint2 sel, uint32_t hb, 
 }
 
 // Inclusive prefix sum over the 64 lanes of a wavefront (DPP row shifts and
-// row broadcasts, 7 adds).
+// row broadcasts, 6 adds).
 __device__ inline uint32_t wave_inclusive_scan(uint32_t v) {
     v += __builtin_amdgcn_update_dpp(0u, v, 0x111, 0xF, 0xF, true);   // row_shr:1
     v += __builtin_amdgcn_update_dpp(0u, v, 0x112, 0xF, 0xF, true);   // row_shr:2
@@ -167,58 +170,73 @@ __device__ inline uint32_t wave_inclusive_scan(uint32_t v) {
     return v;
 }
 
-// Number of set bits of each byte of x, one count per byte.
-__device__ inline uint32_t byte_popcounts(uint32_t x) {
+// Number of set bits of each 4-bit nibble of x, one count per nibble.
+__device__ inline uint32_t nibble_popcounts(uint32_t x) {
     x = x - ((x >> 1) & 0x55555555u);
-    x = (x & 0x33333333u) + ((x >> 2) & 0x33333333u);
-    return (x + (x >> 4)) & 0x0F0F0F0Fu;
+    return (x & 0x33333333u) + ((x >> 2) & 0x33333333u);
 }
 
-// Per-tile decode state of one lane: exclusive prefix (over lanes) of the kept
-// counts of every step, as three words of 10-bit fields, and the start (in
-// halfs) of every step's block of values.
-struct StepOffsets {
-    uint32_t excl[3];
-    uint32_t base[kSteps];  // wavefront-uniform
+// Per-record decode state of one lane, from its mask word (byte s = step s).
+// The record's values are 16 blocks, b = 2 s + h for step s and nibble half h
+// (h = 0: positions 0-3, h = 1: positions 4-7), each holding the 64 lanes'
+// values of that nibble in lane order. A lane's nibble (s, h) therefore starts
+// at the block's start plus the lane's exclusive prefix of the block's kept
+// counts: four DPP scans over 8-bit fields give every lane its prefix for all
+// 16 blocks (at most 63 x 4 = 252, so the fields never carry), and lane 63's
+// prefix plus its own count gives each block's size.
+struct RecState {
+    uint32_t excl[4];            // prefixes: [2 (s / 4) + h], field s % 4
+    uint32_t base2[2 * kSteps];  // byte offset of block b (wavefront-uniform)
+    uint32_t t[4];               // selector-table offsets (nibble x 8): [2 (s / 4) + h], byte s % 4
 };
 
-__device__ inline StepOffsets step_offsets(uint2 msk) {
-    const uint32_t bl = byte_popcounts(msk.x), bh = byte_popcounts(msk.y);
-    uint32_t w[3];
-    w[0] = (bl & 0xFFu) | ((bl & 0xFF00u) << 2) | ((bl & 0xFF0000u) << 4);
-    w[1] = (bl >> 24) | ((bh & 0xFFu) << 10) | ((bh & 0xFF00u) << 12);
-    w[2] = ((bh >> 16) & 0xFFu) | ((bh >> 24) << 10);
-    StepOffsets o;
+__device__ inline RecState rec_state(uint2 msk) {
+    const uint32_t nx = nibble_popcounts(msk.x), ny = nibble_popcounts(msk.y);
+    const uint32_t w[4] = {nx & 0x0F0F0F0Fu, (nx >> 4) & 0x0F0F0F0Fu, ny & 0x0F0F0F0Fu, (ny >> 4) & 0x0F0F0F0Fu};
+    RecState o;
+    uint32_t tot[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        uint32_t inc = wave_inclusive_scan(w[i]);
+        asm("" : "+v"(inc));     // keeps the scan's last add a DPP add (the optimizer would split it)
+        o.excl[i] = inc - w[i];  // exact: lane 63's inclusive sum may carry, the difference does not
+        // Block sizes: lane 63's prefix plus its own count, per field (up to 256), in 16-bit halves.
+        const uint32_t x = __builtin_amdgcn_readlane(o.excl[i], 63), c = __builtin_amdgcn_readlane(w[i], 63);
+        const uint32_t even = (x & 0x00FF00FFu) + (c & 0x00FF00FFu), odd = ((x >> 8) & 0x00FF00FFu) + ((c >> 8) & 0x00FF00FFu);
+        tot[i][0] = even & 0xFFFFu;
+        tot[i][1] = odd & 0xFFFFu;
+        tot[i][2] = even >> 16;
+        tot[i][3] = odd >> 16;
+    }
     uint32_t run = 0;
 #pragma unroll
-    for (int i = 0; i < 3; ++i) {
-        const uint32_t inc = wave_inclusive_scan(w[i]);
-        o.excl[i] = inc - w[i];
-        const uint32_t tot = __builtin_amdgcn_readlane(inc, 63);
+    for (int st = 0; st < kSteps; ++st) {
 #pragma unroll
-        for (int f = 0; f < 3; ++f) {
-            const int st = 3 * i + f;
-            if (st < kSteps) {
-                o.base[st] = run;
-                run += (tot >> (10 * f)) & 0x3FFu;
-            }
+        for (int h = 0; h < 2; ++h) {
+            o.base2[2 * st + h] = 2 * run;
+            run += tot[2 * (st >> 2) + h][st & 3];
         }
     }
+    uint32_t t0 = (msk.x << 3) & 0x78787878u, t1 = (msk.x >> 1) & 0x78787878u;
+    uint32_t t2 = (msk.y << 3) & 0x78787878u, t3 = (msk.y >> 1) & 0x78787878u;
+    // Opaque to the optimizer: a step's selector index is then one bit-field
+    // extract of these words instead of a shift and a mask of the raw mask.
+    asm("" : "+v"(t0), "+v"(t1), "+v"(t2), "+v"(t3));
+    o.t[0] = t0;
+    o.t[1] = t1;
+    o.t[2] = t2;
+    o.t[3] = t3;
     return o;
 }
 
-// Issues the LDS reads of step s of the staged tile.
-// tlo/thi: mask bytes of the step's low / high nibbles pre-scaled by 8.
-__device__ inline StepWords read_step(lds_u32 *region, const uint8_t *lut, const StepOffsets &so,
-                                      uint32_t tlo, uint32_t thi, int s) {
+// Issues the LDS reads of step s of the staged record.
+__device__ inline StepWords read_step(lds_u32 *region, const uint8_t *lut, const RecState &rs, int s) {
     StepWords w;
-    const uint32_t P = (so.excl[s / 3] >> (10 * (s % 3))) & 0x3FFu;
-    const int sh = 8 * (s & 3);
-    const uint32_t i0 = (tlo >> sh) & 0xFFu, i1 = (thi >> sh) & 0xFFu;
-    w.hb[0] = (P + so.base[s]) << 1;
-    w.hb[1] = w.hb[0] + 2u * (uint32_t)__builtin_popcount(i0);
-    read_nibble(region, w.hb[0], i0, lut, w.e, w.sel[0]);
-    read_nibble(region, w.hb[1], i1, lut, w.e + 3, w.sel[1]);
+    const int f = 8 * (s & 3), q = 2 * (s >> 2);
+    w.hb[0] = 2 * ((rs.excl[q] >> f) & 0xFFu) + rs.base2[2 * s];
+    w.hb[1] = 2 * ((rs.excl[q + 1] >> f) & 0xFFu) + rs.base2[2 * s + 1];
+    read_nibble(region, w.hb[0], (rs.t[q] >> f) & 0xFFu, lut, w.e, w.sel[0]);
+    read_nibble(region, w.hb[1], (rs.t[q + 1] >> f) & 0xFFu, lut, w.e + 3, w.sel[1]);
     return w;
 }
 
@@ -230,9 +248,8 @@ __device__ inline half8 finish_step(const StepWords &w) {
     return __builtin_bit_cast(half8, a);
 }
 
-__device__ inline half8 decode_step(lds_u32 *region, const uint8_t *lut, const StepOffsets &so,
-                                    uint32_t tlo, uint32_t thi, int s) {
-    return finish_step(read_step(region, lut, so, tlo, thi, s));
+__device__ inline half8 decode_step(lds_u32 *region, const uint8_t *lut, const RecState &rs, int s) {
+    return finish_step(read_step(region, lut, rs, s));
 }
 
 // One 16-byte chunk X[n][k..k+7] of the X tile, zero outside N x K.
@@ -343,18 +360,13 @@ __device__ inline void stage_tile(const TileRegs<NT> &r, uint8_t *xs, uint8_t *r
 template <int NT>
 __device__ inline void compute_tile(lds_u32 *region, const uint8_t *xs, const uint8_t *lut, uint2 msk, int lane,
                                     floatx4 (&acc)[NT]) {
-    const StepOffsets so = step_offsets(msk);
-    // Low / high nibble of every mask byte, times 8 (selector table offsets),
-    // opaque to the optimizer so that a step's index is one bit-field extract.
-    uint32_t tlo0 = (msk.x << 3) & 0x78787878u, thi0 = (msk.x >> 1) & 0x78787878u;
-    uint32_t tlo1 = (msk.y << 3) & 0x78787878u, thi1 = (msk.y >> 1) & 0x78787878u;
-    asm("" : "+v"(tlo0), "+v"(thi0), "+v"(tlo1), "+v"(thi1));
+    const RecState rs = rec_state(msk);
     const uint8_t *xb = xs + (lane & 15) * kXRowBytes + 16 * (lane >> 4);
-    StepWords cur = read_step(region, lut, so, tlo0, thi0, 0);
+    StepWords cur = read_step(region, lut, rs, 0);
 #pragma unroll
     for (int s = 0; s < kSteps; ++s) {
         StepWords nxt;
-        if (s + 1 < kSteps) nxt = read_step(region, lut, so, s + 1 < 4 ? tlo0 : tlo1, s + 1 < 4 ? thi0 : thi1, s + 1);
+        if (s + 1 < kSteps) nxt = read_step(region, lut, rs, s + 1);
         half8 bv[NT];
 #pragma unroll
         for (int nb = 0; nb < NT; ++nb) bv[nb] = *reinterpret_cast<const half8 *>(xb + nb * 16 * kXRowBytes + 64 * s);
@@ -666,16 +678,11 @@ constexpr int kDecodeAheadMinBlocks = 3;
 template <int NB>
 __device__ inline void decode_record(lds_u32 *slot, const uint8_t *lut, uint2 msk, const v4u32 (&xb)[NB][kSteps],
                                      floatx4 (&acc)[NB]) {
-    const StepOffsets so = step_offsets(msk);
-    uint32_t tlo0 = (msk.x << 3) & 0x78787878u, thi0 = (msk.x >> 1) & 0x78787878u;
-    uint32_t tlo1 = (msk.y << 3) & 0x78787878u, thi1 = (msk.y >> 1) & 0x78787878u;
-    // Opaque to the optimizer: a step's selector index is then one bit-field
-    // extract of these words instead of a shift and a mask of the raw mask.
-    asm("" : "+v"(tlo0), "+v"(thi0), "+v"(tlo1), "+v"(thi1));
+    const RecState rs = rec_state(msk);
     if (NB >= kDecodeAheadMinBlocks) {  // every step's LDS reads first: a short dependency chain per record
         StepWords all[kSteps];
 #pragma unroll
-        for (int s = 0; s < kSteps; ++s) all[s] = read_step(slot, lut, so, s < 4 ? tlo0 : tlo1, s < 4 ? thi0 : thi1, s);
+        for (int s = 0; s < kSteps; ++s) all[s] = read_step(slot, lut, rs, s);
 #pragma unroll
         for (int s = 0; s < kSteps; ++s) {
             const half8 av = finish_step(all[s]);
@@ -685,11 +692,11 @@ __device__ inline void decode_record(lds_u32 *slot, const uint8_t *lut, uint2 ms
         }
         return;
     }
-    StepWords sw = read_step(slot, lut, so, tlo0, thi0, 0);
+    StepWords sw = read_step(slot, lut, rs, 0);
 #pragma unroll
     for (int s = 0; s < kSteps; ++s) {
         StepWords nx;
-        if (s + 1 < kSteps) nx = read_step(slot, lut, so, s + 1 < 4 ? tlo0 : tlo1, s + 1 < 4 ? thi0 : thi1, s + 1);
+        if (s + 1 < kSteps) nx = read_step(slot, lut, rs, s + 1);
         const half8 av = finish_step(sw);
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
@@ -960,12 +967,21 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
         }
 #pragma unroll
         for (int r = 0; r < R; ++r) {
+            // The next unit's X is requested first in the unit, ahead of every
+            // record it will be used with: loads complete in issue order, so a
+            // later request would make the next unit's first decode wait for the
+            // records issued before it as well.
+            if (kXAhead && r == 0) {
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb) fetch_x(a, xr, xoff[nb], kp, lane, xn[kXAhead ? nb : 0]);
+            }
             // Arrival at the row set finished by the previous unit: its partial's
-            // stores were followed by record R-1's L + 1 loads (and the offsets
-            // load, which this count conservatively waits for too); the counter's
-            // answer is read a record or two later, so waiting for it stalls nothing.
+            // stores were followed by the offsets load, the next unit's X (8 loads
+            // per token block, when prefetched) and record R-1's L + 1 loads; the
+            // counter's answer is read a record or two later, so waiting for it
+            // stalls nothing.
             if (r == 1 && pend_set >= 0) {
-                __builtin_amdgcn_s_waitcnt(vmcnt_only(L + 1));
+                __builtin_amdgcn_s_waitcnt(vmcnt_only(kXAhead ? L + 2 + kSteps * NB : L + 1));
                 old = arrive_count(a, pend_set, lane, g);
             }
             if (r == R - 1 && pend_set >= 0) {
@@ -978,10 +994,6 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
             else
                 dma_rec<L>(stream, __builtin_amdgcn_readlane(on, r - 1), __builtin_amdgcn_readlane(on, R + r - 1), lane,
                            slots[r - 1], msk[r - 1]);
-            if (kXAhead && r == 2) {
-#pragma unroll
-                for (int nb = 0; nb < NB; ++nb) fetch_x(a, xr, xoff[nb], kp, lane, xn[kXAhead ? nb : 0]);
-            }
             decode_record<NB>(as_lds(slots[r]), lut, msk[r], xb, acc[r]);
         }
         if (!kXAhead) {
@@ -1144,16 +1156,11 @@ __global__ __launch_bounds__(64) void densify_kernel(const uint8_t *stream, cons
     const uint4 *vp = reinterpret_cast<const uint4 *>(rec + kMaskBytes);
     for (int c = lane; c < nch; c += kLanes) reinterpret_cast<uint4 *>(region)[c] = vp[c];
     __syncthreads();
-    const StepOffsets so = step_offsets(msk);
-    uint32_t tlo0 = (msk.x << 3) & 0x78787878u, thi0 = (msk.x >> 1) & 0x78787878u;
-    uint32_t tlo1 = (msk.y << 3) & 0x78787878u, thi1 = (msk.y >> 1) & 0x78787878u;
-    // Opaque to the optimizer: a step's selector index is then one bit-field
-    // extract of these words instead of a shift and a mask of the raw mask.
-    asm("" : "+v"(tlo0), "+v"(thi0), "+v"(tlo1), "+v"(thi1));
+    const RecState rs = rec_state(msk);
     const int64_t row = rb * kTileRows + (lane & 15);
     if (row >= M) return;
     for (int s = 0; s < kSteps; ++s) {
-        const half8 av = decode_step(as_lds(region), lut, so, s < 4 ? tlo0 : tlo1, s < 4 ? thi0 : thi1, s);
+        const half8 av = decode_step(as_lds(region), lut, rs, s);
         const uint4 u = __builtin_bit_cast(uint4, av);
         const int64_t col = kt * kTileK + tile_col(lane >> 4, s, 0);
         uint16_t *dst = Wd + row * ldw + col;

@@ -74,7 +74,8 @@ def test_roundtrip_workloads(hlib):
 
 
 def test_record_layout_matches_definition(hlib):
-    """Decode one record by hand from its documented layout (lane-major mask bytes, step-major values)."""
+    """Decode one record by hand from its documented layout: lane-major mask bytes; values in
+    blocks of (step, nibble half), lanes in order within a block."""
     import ctypes
     rng = np.random.default_rng(5)
     M, K = 16, 256
@@ -92,11 +93,15 @@ def test_record_layout_matches_definition(hlib):
             r, g = lane % 16, lane // 16
             byte = stream[8 * lane + s]
             for j in range(8):
-                k = 32 * s + 8 * g + j
-                assert ((byte >> j) & 1) == mask[r, k]
-                if mask[r, k]:
-                    assert vals[v] == W[r, k]
-                    v += 1
+                assert ((byte >> j) & 1) == mask[r, 32 * s + 8 * g + j]
+        for h in range(2):
+            for lane in range(64):
+                r, g = lane % 16, lane // 16
+                for j in range(4 * h, 4 * h + 4):
+                    k = 32 * s + 8 * g + j
+                    if mask[r, k]:
+                        assert vals[v] == W[r, k]
+                        v += 1
     assert v == mask.sum()
     assert np.all(stream[512 + 2 * v:] == 0)
 

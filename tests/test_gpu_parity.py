@@ -89,7 +89,7 @@ def test_decode_roundtrip_through_device(torch, usp):
     A.free()
     assert np.array_equal(Wo, oracle.masked_bits(W, mask))
     assert np.array_equal(mo, mask)
-    assert info["nnz"] == int(mask.sum()) and info["format_version"] == 1
+    assert info["nnz"] == int(mask.sum()) and info["format_version"] == 2
 
 
 def test_tiny_workload_parity(torch, usp):
@@ -720,3 +720,45 @@ def test_freed_handle_rejected(torch, usp):
     assert "freed" in usp.usp_last_error()
     assert lib.usp_free(h) == 1
     assert lib.usp_workspace_size(h, 16) == 0
+
+
+# Stress of the split-K protocol (partials stored with device-coherent stores,
+# an arrival counter, the last arrival summing every slot in order): one graph
+# holding a split product is replayed 2000 times for each split route, each
+# replay compared bit for bit with the eager result, stopping at the first
+# mismatch (checked on the device after every replay, read back every 250
+# replays). Routes: column-chunk (5120 x 5120 at 16 tokens: 5 chunks per row
+# block; at 32 tokens with two token blocks), direct-to-LDS (28672 x 8192 at 16
+# and 64 tokens, row sets split over wavefronts), four-wavefront (4101 x 1000 at
+# 48 tokens, row groups split over workgroups).
+@pytest.mark.parametrize("M,K,N", [(5120, 5120, 16), (5120, 5120, 32), (28672, 8192, 16), (28672, 8192, 64),
+                                   (4101, 1000, 48)])
+def test_split_protocol_stress(torch, usp, M, K, N):
+    W, mask, X = wl.make_random(M, K, N, 0.5, seed=700 + N)
+    A = usp.SparseMatrix(W, mask)
+    print(f"case M={M} K={K} N={N}: {A.plan(N)}", flush=True)
+    assert A.workspace_size(N) > 0  # a split route
+    Xd = to_dev(torch, X)
+    ws = A.make_workspace(N)
+    Ye = A.spmm(Xd, workspace=A.make_workspace(N))
+    Yg = torch.empty_like(Ye)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        A.spmm(Xd, Yg, workspace=ws)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        A.spmm(Xd, Yg, workspace=ws)
+    ok = torch.ones((), dtype=torch.bool, device="cuda")
+    for rep in range(2000):
+        Yg.zero_()  # eager work between replays; a replay that skipped an output would leave a zero
+        g.replay()
+        ok &= (Yg.view(torch.int16) == Ye.view(torch.int16)).all()
+        if rep % 250 == 249:
+            torch.cuda.synchronize()
+            assert bool(ok), (M, K, N, rep)
+    torch.cuda.synchronize()
+    assert bool(ok)
+    A.free()
