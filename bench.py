@@ -188,10 +188,11 @@ def hipblaslt_best(torch, M, K, N, Wds, X, steps, warmup, max_algos=16):
     ws = torch.empty(max(1, max(lib.usp_dense_workspace(ctx, i) for i in range(n.value))), dtype=torch.uint8,
                      device="cuda")
     Yd = torch.empty((N, M), dtype=torch.float16, device="cuda")
-    st = torch.cuda.current_stream().cuda_stream
 
     def fns(i):
         def run(Wx):
+            # The stream is read at call time: under graph capture it is the capturing stream.
+            st = torch.cuda.current_stream().cuda_stream
             rc = lib.usp_dense_run(ctx, i, Wx.data_ptr(), X.data_ptr(), Yd.data_ptr(), ws.data_ptr(), ws.numel(), st)
             if rc != 0:
                 raise RuntimeError(f"hipblasLtMatmul returned {rc}")
@@ -213,6 +214,9 @@ def hipblaslt_best(torch, M, K, N, Wds, X, steps, warmup, max_algos=16):
         graph_ms = timed_steps(torch, fns(best), steps, warmup, "graph")
     except Exception:  # capture not supported by this algorithm: the eager time stands
         pass
+    if graph_ms is not None and graph_ms < 0.5 * best_ms:
+        raise RuntimeError(f"hipBLASLt graph replay {graph_ms * 1e3:.2f} us against {best_ms * 1e3:.2f} us eager: "
+                           "the captured graph cannot be doing the work")
     fns(best)[0]()
     ref = torch.matmul(X, Wds[0].t())
     torch.cuda.synchronize()

@@ -844,6 +844,14 @@ __global__ __launch_bounds__(W * kLanes) void spmm_chunk_kernel(WaveArgs a, cons
 
 constexpr int kDmaRows = 4;  // row blocks per unit = LDS slots
 
+// Whether records travel into LDS whole, mask bytes included (one and two
+// token blocks, two wavefronts per SIMD), or the mask word of each lane comes
+// by its own load into registers (three and four blocks, one wavefront per
+// SIMD, where reading the mask from LDS would put one more LDS round trip in
+// front of every record's decode: 107.6 against 104.1 us on the 70B FFN layer
+// at 64 tokens).
+__host__ __device__ constexpr bool dma_mask_in_lds(int nb) { return nb <= 2; }
+
 // Encoding of s_waitcnt that waits until at most n vector memory operations
 // are outstanding and ignores the other counters.
 __device__ constexpr int vmcnt_only(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0F70; }
@@ -861,18 +869,33 @@ __device__ inline uint32_t unit_offsets(const WaveArgs &a, __amdgpu_buffer_rsrc_
     return __builtin_amdgcn_raw_buffer_load_b32(offr, byte, 0, 0);
 }
 
-// Loads the record at 16-byte units [o0, o1) into an LDS slot (L transfers of
-// 16 bytes per lane) and this lane's mask word into msk.
-template <int L>
+// Loads the whole record at 16-byte units [o0, o1), mask bytes and values,
+// into an LDS slot: L transfers of 16 bytes per lane. The mask comes with the
+// values rather than by a separate load into registers: the compiler's wait
+// for such a load at the top of the unit loop (merged over the loop's entry
+// and back edge) also waited for the next record, which cost ~6% on the 70B
+// FFN layer.
+// Without MASK_IN_LDS the slot receives the values only and msk this lane's
+// mask word.
+template <int L, bool MASK_IN_LDS>
 __device__ inline void dma_rec(const uint8_t *__restrict__ stream, uint32_t o0, uint32_t o1, int lane,
                                uint8_t *slot, uint2 &msk) {
     const __amdgpu_buffer_rsrc_t rec = __builtin_amdgcn_make_buffer_rsrc(
         (void *)(stream + (uint64_t)o0 * 16), (short)0, (int)((o1 - o0) * 16), kBufferRsrcWord3);
-    msk = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rec, lane * 8, 0, 0));
+    constexpr int first = MASK_IN_LDS ? 0 : kMaskBytes;
+    if (!MASK_IN_LDS) msk = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rec, lane * 8, 0, 0));
 #pragma unroll
     for (int i = 0; i < L; ++i)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rec, (__attribute__((address_space(3))) void *)(slot + 1024 * i), 16,
-                                                 kMaskBytes + 1024 * i + lane * 16, 0, 0, 0);
+                                                 first + 1024 * i + lane * 16, 0, 0, 0);
+}
+
+// This lane's mask word of the record staged in `slot`.
+__device__ inline uint2 slot_mask(const uint8_t *slot, int lane) {
+    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+    typedef const __attribute__((address_space(3))) u32x2 lds_u32x2;
+    const u32x2 m = ((lds_u32x2 *)(const __attribute__((address_space(3))) void *)slot)[lane];
+    return make_uint2(m.x, m.y);
 }
 
 
@@ -881,7 +904,9 @@ template <int L, int NB>
 __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint32_t *__restrict__ off,
                                                          const uint8_t *__restrict__ stream) {
     constexpr int R = kDmaRows;
-    constexpr int kSlot = 1024 * L + 16;  // values + the decode's 12-byte overread
+    constexpr bool kMaskInLds = dma_mask_in_lds(NB);
+    constexpr int kValues = kMaskInLds ? kMaskBytes : 0;  // where the values start in a slot
+    constexpr int kSlot = 1024 * L + 16;  // (mask bytes,) values and the decode's 12-byte overread
     __shared__ __attribute__((aligned(16))) uint8_t slot0[kSlot];
     __shared__ __attribute__((aligned(16))) uint8_t slot1[kSlot];
     __shared__ __attribute__((aligned(16))) uint8_t slot2[kSlot];
@@ -916,7 +941,7 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
         for (int nb = 0; nb < NB; ++nb) acc[r][nb] = floatx4{0.f, 0.f, 0.f, 0.f};
     int64_t set = u0 / a.KT, kt = u0 % a.KT;
     int64_t pend_set = -1, pend_nseg = 0;  // partial stored, arrival not yet counted
-    uint2 msk[R];
+    uint2 msk[R];  // mask words, when they come by their own loads
     const __amdgpu_buffer_rsrc_t offr = __builtin_amdgcn_make_buffer_rsrc(
         (void *)off, (short)0, (int)((a.RB * a.KT + 1) * 4), kBufferRsrcWord3);
     // The first unit's records 0..R-2 and X; record R-1 is requested while record 0
@@ -931,14 +956,35 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
         }
         on = unit_offsets(a, offr, s1, k1, lane, u0 + 1 < u1);
     }
+    // With whole records in LDS, X first: the compiler's wait counts at the
+    // loop head merge this path with the loop's own, where X is older than
+    // every record in flight. With separate mask loads (3-4 token blocks, 32 KB
+    // of X per wavefront) the records first: 104 against 107 us on the 70B FFN
+    // layer at 64 tokens.
+    v4u32 xb[NB][kSteps];
+    if (kMaskInLds) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) fetch_x(a, xr, xoff[nb], kt, lane, xb[nb]);
+    }
 #pragma unroll
     for (int r = 0; r < R - 1; ++r)
-        dma_rec<L>(stream, __builtin_amdgcn_readlane(oc, r), __builtin_amdgcn_readlane(oc, R + r), lane, slots[r],
-                   msk[r]);
-    v4u32 xb[NB][kSteps];
+        dma_rec<L, kMaskInLds>(stream, __builtin_amdgcn_readlane(oc, r), __builtin_amdgcn_readlane(oc, R + r), lane,
+                               slots[r], msk[r]);
+    if (!kMaskInLds) {
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) fetch_x(a, xr, xoff[nb], kt, lane, xb[nb]);
+        for (int nb = 0; nb < NB; ++nb) fetch_x(a, xr, xoff[nb], kt, lane, xb[nb]);
+    }
     for (int64_t u = u0; u < u1; ++u) {
+        // Two wavefronts share most SIMDs, and issue arbitration favours the
+        // older: with equal ranges the younger finished ~5 us after it (70B FFN
+        // layer, 16 tokens). Raising the priority on every other unit gives both
+        // about the same share of issue slots.
+        if (NB <= 2) {
+            if (u & 1)
+                __builtin_amdgcn_s_setprio(1);
+            else
+                __builtin_amdgcn_s_setprio(0);
+        }
         int64_t setn = set, ktn = kt + 1;
         if (ktn == a.KT) {
             ktn = 0;
@@ -977,11 +1023,11 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
             }
             // Arrival at the row set finished by the previous unit: its partial's
             // stores were followed by the offsets load, the next unit's X (8 loads
-            // per token block, when prefetched) and record R-1's L + 1 loads; the
-            // counter's answer is read a record or two later, so waiting for it
-            // stalls nothing.
+            // per token block, when prefetched) and record R-1's L (+ 1 for a
+            // separate mask) loads; the counter's answer is read a record or two
+            // later, so waiting for it stalls nothing.
             if (r == 1 && pend_set >= 0) {
-                __builtin_amdgcn_s_waitcnt(vmcnt_only(kXAhead ? L + 2 + kSteps * NB : L + 1));
+                __builtin_amdgcn_s_waitcnt(vmcnt_only(kXAhead ? L + (kMaskInLds ? 1 : 2) + kSteps * NB : L + 1));
                 old = arrive_count(a, pend_set, lane, g);
             }
             if (r == R - 1 && pend_set >= 0) {
@@ -989,12 +1035,13 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
                 pend_set = -1;
             }
             if (r == 0)
-                dma_rec<L>(stream, __builtin_amdgcn_readlane(oc, R - 1), __builtin_amdgcn_readlane(oc, 2 * R - 1), lane,
-                           slots[R - 1], msk[R - 1]);
+                dma_rec<L, kMaskInLds>(stream, __builtin_amdgcn_readlane(oc, R - 1),
+                                       __builtin_amdgcn_readlane(oc, 2 * R - 1), lane, slots[R - 1], msk[R - 1]);
             else
-                dma_rec<L>(stream, __builtin_amdgcn_readlane(on, r - 1), __builtin_amdgcn_readlane(on, R + r - 1), lane,
-                           slots[r - 1], msk[r - 1]);
-            decode_record<NB>(as_lds(slots[r]), lut, msk[r], xb, acc[r]);
+                dma_rec<L, kMaskInLds>(stream, __builtin_amdgcn_readlane(on, r - 1),
+                                       __builtin_amdgcn_readlane(on, R + r - 1), lane, slots[r - 1], msk[r - 1]);
+            decode_record<NB>(as_lds(slots[r] + kValues), lut, kMaskInLds ? slot_mask(slots[r], lane) : msk[r], xb,
+                              acc[r]);
         }
         if (!kXAhead) {
 #pragma unroll
@@ -1251,9 +1298,18 @@ constexpr int kMinWaveLoads = 2;  // record load groups instantiated: 2..8
 // partial.
 constexpr int64_t kMinUnitsPerDmaWave = 2;
 
-// Record load groups (1 KB each) that cover every record of A.
+// Record load groups (1 KB each) that cover the values of every record of A.
 static int wave_loads(const usp_matrix *A) {
     const int l = (int)ceil_div(A->max_chunks, kLanes);
+    return l < kMinWaveLoads ? kMinWaveLoads : l;
+}
+
+// Load groups of the direct-to-LDS kernel: at one or two token blocks it moves
+// whole records (mask bytes and values) into LDS, otherwise the values only;
+// more than kMaxWaveLoads (records of nearly dense tiles) leaves the kernel out.
+constexpr int kMaxWaveLoads = 8;
+static int dma_loads(const usp_matrix *A, int nb) {
+    const int l = (int)ceil_div((dma_mask_in_lds(nb) ? kMaskChunks : 0) + A->max_chunks, kLanes);
     return l < kMinWaveLoads ? kMinWaveLoads : l;
 }
 
@@ -1404,7 +1460,8 @@ static WaveKind wave_kind(const usp_matrix *A, int loads, int64_t N) {
     if (nb <= kMaxDmaTokenBlocks * kMaxDmaTokenGroups) {
         int nbw, tg;
         dma_tokens(N, nbw, tg);
-        const int64_t slots = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(loads, nbw);
+        const int dl = dma_loads(A, nbw);
+        const int64_t slots = dl > kMaxWaveLoads ? 0 : (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_waves(dl, nbw);
         const int64_t sets = ceil_div(A->RB, kDmaRows);
         // At 3-4 blocks (one wavefront per SIMD, 16 KB partials per row set at
         // 64 tokens) a row set split over more than 4 wavefronts costs more than
@@ -1412,7 +1469,7 @@ static WaveKind wave_kind(const usp_matrix *A, int loads, int64_t N) {
         // 128 row sets over 1024 wavefronts) takes 107.9 us against 101.3 at 64
         // tokens, while the up projection (448 row sets) gains.
         const bool split_ok = nbw < 3 || sets * kMaxDmaWideSplit >= slots / tg;
-        if (split_ok && sets * A->KT >= kDmaUnitsPerSlot * (slots / tg)) return kWaveDma4;
+        if (slots > 0 && split_ok && sets * A->KT >= kDmaUnitsPerSlot * (slots / tg)) return kWaveDma4;
     }
     // The row-block kernel for few long row blocks only while each has few
     // column tiles or the tokens are few: one GPU's share of the 70B FFN
@@ -1471,6 +1528,7 @@ static WavePlan plan_wave(const usp_matrix *A, int64_t N) {
         return p;
     }
     dma_tokens(N, p.nb, p.tg);
+    p.loads = dma_loads(A, p.nb);
     p.rows = kDmaRows;
     p.sets = ceil_div(A->RB, p.rows);
     p.units = p.sets * A->KT;
