@@ -337,6 +337,31 @@ def expected_surplus_fraction(p: float) -> float:
     return expected_surplus_per_window(p) / (4 * p)
 
 
+def sparse_mfma_windows(mask: np.ndarray, rows: int = 16, k: int = 64) -> dict:
+    """How a mask maps onto 2:4 sparse matrix-core operands (Sections 3.2, 4.3).
+
+    A sparse MFMA of the 16 x 64 operand shape takes at most 2 kept entries in
+    every 4 consecutive k of every row. Returns the share of 4-wide windows by
+    kept count (0..4) and the share of rows x k blocks whose windows all hold at
+    most 2, i.e. blocks one sparse operand covers; every other block needs a
+    second operand for its windows' 3rd and 4th entries.
+    """
+    m = np.asarray(mask, dtype=np.uint8)
+    R = m.shape[0] - m.shape[0] % rows
+    C = m.shape[1] - m.shape[1] % k
+    win = m[:R, :C].reshape(R, C // 4, 4).sum(axis=2)
+    dist = np.bincount(win.ravel(), minlength=5)[:5] / win.size
+    worst = win.reshape(R // rows, rows, C // k, k // 4).max(axis=(1, 3))
+    return {"window_kept_share": [float(x) for x in dist], "share_over_2": float(dist[3] + dist[4]),
+            "blocks_one_operand": float((worst <= 2).mean()), "blocks": int(worst.size)}
+
+
+def expected_one_operand_blocks(p: float, rows: int = 16, k: int = 64) -> float:
+    """Independent keep decisions with probability p: a block of rows x k/4
+    windows fits one 2:4 operand when no window keeps 3 or 4 entries."""
+    return (1 - 4 * p ** 3 * (1 - p) - p ** 4) ** (rows * k // 4)
+
+
 # ---------------------------------------------------------------------------
 # Report over the workload set (run as a module)
 # ---------------------------------------------------------------------------
@@ -344,6 +369,8 @@ def expected_surplus_fraction(p: float) -> float:
 def _report(argv=None) -> int:
     ap = argparse.ArgumentParser(description="Three-layer format statistics on the synthetic workload masks")
     ap.add_argument("--bands", type=int, default=4, help="64-row bands sampled per matrix")
+    ap.add_argument("--sparse-mfma", action="store_true",
+                    help="2:4 window statistics (sparse_mfma_windows) on the first 4096 rows instead")
     args = ap.parse_args(argv)
     import workloads as wl
     rng = np.random.default_rng(0)
@@ -354,8 +381,12 @@ def _report(argv=None) -> int:
         for s in cfg["sparsity"]:
             mask = wl.make_mask(cfg, W, s)
             t0 = time.perf_counter()
-            st = sample_stats(W, mask, bands)
-            st.update(workload=name, sparsity_pct=s, bands=bands, seconds=time.perf_counter() - t0)
+            if args.sparse_mfma:
+                st = sparse_mfma_windows(mask[:4096])
+            else:
+                st = sample_stats(W, mask, bands)
+                st.update(bands=bands)
+            st.update(workload=name, sparsity_pct=s, seconds=time.perf_counter() - t0)
             print(json.dumps(st), flush=True)
     return 0
 

@@ -162,3 +162,28 @@ def test_storage_bounds_and_workload_statistics():
     assert st["bytes_per_position"] >= 1.125
     assert 0.15 < st["slot_filling_frac"] < 0.21
     assert st["residual_frac"] < 0.02
+
+
+# 2:4 window statistics of the sparse matrix-core operand shape (16 x 64).
+def test_sparse_mfma_windows_pins():
+    import numpy as np
+    from paper_2607_08786_amd import three_layer as tl
+    # An exact 2:4 mask: every window keeps its first two entries; one operand covers every block.
+    m = np.tile(np.array([1, 1, 0, 0], dtype=np.uint8), (32, 32))
+    st = tl.sparse_mfma_windows(m)
+    assert st["window_kept_share"] == [0.0, 0.0, 1.0, 0.0, 0.0] and st["blocks_one_operand"] == 1.0
+    # One window with 3 kept entries spoils exactly its own block.
+    m2 = m.copy()
+    m2[17, 64 + 2] = 1
+    st2 = tl.sparse_mfma_windows(m2)
+    assert st2["blocks"] == 4 and st2["blocks_one_operand"] == 0.75
+    # Independent keep decisions: the window histogram is Binomial(4, p), and the closed form of
+    # the one-operand share matches a large random mask at a density where it is not ~0.
+    rng = np.random.default_rng(5)
+    for p in (0.5, 0.05):
+        mm = (rng.random((4096, 1024)) < p).astype(np.uint8)
+        st3 = tl.sparse_mfma_windows(mm)
+        binom = [1 * (1 - p) ** 4, 4 * p * (1 - p) ** 3, 6 * p ** 2 * (1 - p) ** 2, 4 * p ** 3 * (1 - p), p ** 4]
+        assert np.allclose(st3["window_kept_share"], binom, atol=3e-3)
+        assert abs(st3["blocks_one_operand"] - tl.expected_one_operand_blocks(p)) < 0.02
+    assert tl.expected_one_operand_blocks(0.5) < 1e-40
