@@ -38,6 +38,7 @@
 #include <cstdio>
 #include <mutex>
 #include <string>
+#include <utility>
 
 #include "usp_internal.h"
 
@@ -546,6 +547,9 @@ struct WaveArgs {
     const uint16_t *res;          // fp16 residual, token n at res + n * ldr, or null
     int64_t ldr;
     int act;                      // usp_activation
+    const uint8_t *xp;            // X packed in product order (pack_x_kernel), or null
+    uint32_t xp_bytes;
+    int tb;                       // blocks of 16 tokens in xp: ceil(N / 16)
 };
 
 // Rows m..m+3 of token n (a lane's MFMA outputs), rounded to fp16 after the
@@ -1109,6 +1113,340 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
 }
 
 // ---------------------------------------------------------------------------
+// Shared-decode kernel (more than 64 tokens, and 33-64 on large layers).
+//
+// A workgroup of four wavefronts streams a contiguous range of units (4 row
+// blocks x 1 column tile). Wavefront j owns row block j of every unit: it
+// moves that record into its own ring of S LDS slots (S - 1 units in flight
+// while one is decoded; S as deep as LDS allows), decodes it once into the 8 A operands of its steps and writes them to a
+// shared LDS buffer; after a barrier every wavefront multiplies all four
+// records' operands with the X of its own slice of tokens (NB blocks of 16,
+// up to 64 tokens, held in registers). Each record is decoded once however
+// many tokens there are: the direct-to-LDS kernel's token groups decoded every
+// record once per group (2 at 128 tokens, 4 at 256). The steps run outermost,
+// so each step's X operands are reloaded for the next unit as soon as its
+// last MFMA has been issued, 7 steps of MFMAs ahead of their use. Split row
+// sets are finished per wavefront through the token-group arrival protocol
+// (counter and partial slices per wavefront).
+// ---------------------------------------------------------------------------
+
+constexpr int kShareWaves = 4;  // wavefronts per workgroup = row blocks per unit
+
+// Workgroup barrier ordering LDS reads and writes only. __syncthreads() is a
+// workgroup fence, and a fence that covers LDS also waits for every
+// direct-to-LDS transfer in flight, which would drain the record ring at every
+// barrier; here this wavefront's LDS instructions complete (lgkmcnt) before
+// the barrier, and the clobber keeps the compiler from moving memory accesses
+// across it. Transfers into a ring slot are only ever read by the wavefront
+// that issued them, behind the compiler's own waits.
+__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// ---------------------------------------------------------------------------
+// X packed in the order the shared-decode kernel's products read it. Read in
+// place, each B-operand load of 64 lanes x 16 bytes touches 16 token rows (64
+// bytes of each, at the row stride of X); the memory pipeline handles such a
+// load at a quarter of the rate of one contiguous kilobyte, and at 64 and more
+// tokens those loads, not the decode or the products, set the shared-decode
+// kernel's pace (measured: the same kernel with contiguous loads of the same
+// count, 152.6 -> 112.9 us on the 70B FFN layer at 128 tokens). One pass
+// before the product rewrites X as blocks of 1 KB: block ((kt * 8 + s) * TB +
+// tb), lane l = 16 g + n, holds X[16 tb + n][256 kt + 32 s + 8 g .. + 7]
+// (zeros past N and K), so every load in the product reads one block.
+// ---------------------------------------------------------------------------
+
+constexpr size_t kPackBlockBytes = 1024;
+static size_t packed_x_bytes(int64_t KT, int64_t N) {
+    return (size_t)KT * kSteps * (size_t)((N + 15) / 16) * kPackBlockBytes;
+}
+
+// One wavefront per (column tile, token block): its 8 steps' blocks. Needs
+// K % 8 == 0, ldx % 8 == 0 and X 16-byte aligned (the single-pass kernels'
+// conditions).
+__global__ __launch_bounds__(kLanes) void pack_x_kernel(const uint16_t *__restrict__ X, int64_t ldx, int N, int64_t K,
+                                                       int TB, uint8_t *__restrict__ xp) {
+    const int lane = threadIdx.x;
+    const int64_t kt = blockIdx.x / TB, tb = blockIdx.x % TB;
+    const int64_t n = 16 * tb + (lane & 15);
+    const int64_t k0 = kt * kTileK + 8 * (lane >> 4);
+    v4u32 v[kSteps];
+#pragma unroll
+    for (int st = 0; st < kSteps; ++st) {
+        const int64_t k = k0 + 32 * st;
+        v[st] = n < N && k < K ? *reinterpret_cast<const v4u32 *>(X + n * ldx + k) : v4u32{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int st = 0; st < kSteps; ++st)
+        reinterpret_cast<v4u32 *>(xp + ((kt * kSteps + st) * TB + tb) * kPackBlockBytes)[lane] = v[st];
+}
+
+// Loads the whole record at 16-byte units [o0, o1) into LDS at byte address
+// `lds` (L transfers of 16 bytes per lane, non-temporal), issued from inline
+// assembly: the compiler neither sees these loads nor waits for them, so the
+// caller waits for them itself (s_waitcnt vmcnt, counting every vector memory
+// instruction issued after them). The compiler's own waits for transfers into
+// LDS arrays it can tell apart are exact only while at most 8 such arrays are in
+// play and their index is a constant; a ring shared by the wavefronts of a
+// workgroup, indexed by wavefront, made it wait for every transfer in flight.
+typedef int v4i32 __attribute__((ext_vector_type(4)));
+template <int L>
+__device__ inline void dma_rec_asm(const uint8_t *__restrict__ stream, uint32_t o0, uint32_t o1, int lane,
+                                   uint32_t lds) {
+    const uint64_t base = reinterpret_cast<uint64_t>(stream) + (uint64_t)o0 * 16;
+    const v4i32 rsrc = {(int)(uint32_t)base, (int)((uint32_t)(base >> 32) & 0xFFFFu), (int)((o1 - o0) * 16),
+                        kBufferRsrcWord3};
+#pragma unroll
+    for (int i = 0; i < L; ++i)
+        asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen nt lds"
+                     :
+                     : "s"(lds + 1024u * i), "v"(1024 * i + lane * 16), "s"(rsrc)
+                     : "memory", "m0");
+}
+
+// Calls f(std::integral_constant<int, P>{}) for P = 0, 1, ...: an unrolled loop
+// whose index is a constant in every copy, however large the body.
+template <class F, int... P>
+__device__ __attribute__((always_inline)) inline void static_for(F &&f, std::integer_sequence<int, P...>) {
+    (f(std::integral_constant<int, P>{}), ...);
+}
+
+// Ring depth of the shared-decode kernel: two slots per wavefront (one unit
+// in flight while one is decoded).
+constexpr int kShareSlots = 2;
+
+template <int L, int NB>
+__global__ __launch_bounds__(kShareWaves *kLanes, NB <= 2 ? 2 : 1) void spmm_share_kernel(WaveArgs a, const uint32_t *__restrict__ off,
+                                                                         const uint8_t *__restrict__ stream) {
+    constexpr int R = kShareWaves;
+    constexpr int S = kShareSlots;
+    constexpr int kSlot = 1024 * L + 16;  // mask bytes, values and the decode's 12-byte overread
+    // One LDS object per ring position: the compiler then waits only for the
+    // transfers into the slot a decode reads.
+    __shared__ __attribute__((aligned(16))) uint8_t ring0[R][kSlot];
+    __shared__ __attribute__((aligned(16))) uint8_t ring1[R][kSlot];
+    __shared__ __attribute__((aligned(16))) uint4 abuf[R][kSteps][kLanes];  // decoded A operands of the unit
+    __shared__ __attribute__((aligned(16))) uint8_t lut[16 * 8];
+    uint8_t *const ring[2] = {ring0[0], ring1[0]};
+    const int lane = threadIdx.x & (kLanes - 1);
+    const int j = __builtin_amdgcn_readfirstlane(threadIdx.x / kLanes);
+    const int64_t w = blockIdx.x, G = gridDim.x;
+    const int64_t u0 = w * a.units / G, u1 = (w + 1) * a.units / G;
+    if (u0 >= u1) return;  // the whole workgroup
+    if (threadIdx.x < 16) reinterpret_cast<uint2 *>(lut)[threadIdx.x] = nibble_selectors((uint32_t)threadIdx.x);
+
+    // X packed in product order: this wavefront's blocks of step st of column
+    // tile kt start at ((kt * kSteps + st) * TB + NB j) KB (blocks past the
+    // tokens are only read by wavefronts that issue no products).
+    const __amdgpu_buffer_rsrc_t xr =
+        __builtin_amdgcn_make_buffer_rsrc((void *)a.xp, (short)0, (int)a.xp_bytes, kBufferRsrcWord3);
+    const __amdgpu_buffer_rsrc_t offr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)off, (short)0, (int)((a.RB * a.KT + 1) * 4), kBufferRsrcWord3);
+    const int n_lane = lane & 15, g4 = 4 * (lane >> 4);
+    const int tok0 = 16 * NB * j;  // first token of this wavefront's slice
+    const bool has_tokens = tok0 < a.N;
+    const int xlane = (NB * j * 64 + lane) * 16;
+    auto x_at = [&](int64_t kx, int st, int nb) -> int {
+        return (int)((kx * kSteps + st) * a.tb + nb) * (int)kPackBlockBytes + xlane;
+    };
+    // Extents of this wavefront's record of the unit at (set, kt): lane 0 its
+    // start, lane 1 its end; empty past the range (real false) or the matrix.
+    auto rec_offsets = [&](int64_t set, int64_t kt, bool real) -> uint32_t {
+        const int64_t rb = set * R + j;
+        const bool ok = real && lane < 2 && rb < a.RB;
+        return __builtin_amdgcn_raw_buffer_load_b32(offr, ok ? (int)((rb * a.KT + kt + lane) * 4) : 0x7FFFFFF0, 0, 0);
+    };
+    auto advance = [&](int64_t &set, int64_t &kt) {
+        if (++kt == a.KT) {
+            kt = 0;
+            ++set;
+        }
+    };
+    auto dma = [&](uint8_t *slot, uint32_t o) {
+        const uint32_t lds = (uint32_t)reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint8_t *)slot);
+        dma_rec_asm<L>(stream, __builtin_amdgcn_readlane(o, 0), __builtin_amdgcn_readlane(o, 1), lane, lds);
+    };
+    // Vector memory instructions issued after this wavefront's transfer of a
+    // unit's record and before its decode, on the path with the fewest: the
+    // transfer is issued at the end of the unit two before; then the next unit's
+    // offset load (1), its X loads (kSteps NB) and its own transfer (L), and this
+    // unit's offset load (1). Waiting until at most one fewer remain outstanding
+    // finishes the transfer (in-order completion); partial stores and arrivals
+    // add instructions, which only makes the wait stricter. In the first unit
+    // the prologue's second transfer, X and the offset load follow it:
+    // L + kSteps NB + 1, the same count.
+    constexpr int kRecWait = kSteps * NB + L + 1 < 63 ? kSteps * NB + L + 1 : 63;
+
+    floatx4 acc[R][NB];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[r][nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // Prologue: the offsets of units u0 .. u0 + 2, the records of u0 and u0 + 1,
+    // then X (the order kRecWait counts). onext: the unit requested at the end
+    // of the current one (two ahead).
+    int64_t set = u0 / a.KT, kt = u0 % a.KT;
+    int64_t la_set = set, la_kt = kt;  // the unit whose offsets are loaded next
+    const uint32_t oa = rec_offsets(la_set, la_kt, true);
+    advance(la_set, la_kt);
+    const uint32_t ob = rec_offsets(la_set, la_kt, u0 + 1 < u1);
+    advance(la_set, la_kt);
+    uint32_t onext = rec_offsets(la_set, la_kt, u0 + 2 < u1);
+    advance(la_set, la_kt);
+    dma(ring[0] + j * kSlot, oa);
+    dma(ring[1] + j * kSlot, ob);
+    // X of the first unit, step by step as the loop loads it (the compiler's
+    // waits at the loop head assume the loop's order on both paths).
+    v4u32 xb[NB][kSteps];
+    {
+#pragma unroll
+        for (int st = 0; st < kSteps; ++st)
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) xb[nb][st] = __builtin_amdgcn_raw_buffer_load_b128(xr, x_at(kt, st, nb), 0, 0);
+    }
+    lds_barrier();  // the selector table
+
+    // A split row set's partial is stored at the end of the unit that finishes
+    // this workgroup's segment; the arrival is counted at the end of the next
+    // unit, once the stores are acknowledged, and the counter's answer used at
+    // the end of the unit after that (the last arrival then sums the partials):
+    // neither wait then stalls. Whatever is pending is settled after the loop.
+    int64_t pend_set = -1, pend_nseg = 0;  // stored, not yet counted
+    int64_t cnt_set = -1, cnt_nseg = 0;    // counted, answer in cnt_old
+    uint32_t cnt_old = 0;
+    // Vector memory instructions issued after a partial's stores and before
+    // its arrival: the transfer at the end of that unit (L), the next unit's
+    // offset load (1) and its X loads (kSteps NB).
+    constexpr int kPartWait = kSteps * NB + L + 1 < 63 ? kSteps * NB + L + 1 : 63;
+    // One unit: par = (uu - u0) mod S is its ring position (a constant in every
+    // unrolled copy).
+    auto unit = [&](int64_t uu, auto parc) __attribute__((always_inline)) {
+        constexpr int par = decltype(parc)::value;
+        uint8_t *const slot = ring[par] + j * kSlot;
+        const uint32_t onn = rec_offsets(la_set, la_kt, uu + 3 < u1);  // requested at the end of the next unit
+        advance(la_set, la_kt);
+        // Decode this wavefront's record of the unit into registers.
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kRecWait) : "memory");
+        half8 af[kSteps];
+        {
+            const RecState rs = rec_state(slot_mask(slot, lane));
+            lds_u32 *const vals = as_lds(slot + kMaskBytes);
+            StepWords sw = read_step(vals, lut, rs, 0);
+#pragma unroll
+            for (int st = 0; st < kSteps; ++st) {
+                StepWords nx;
+                if (st + 1 < kSteps) nx = read_step(vals, lut, rs, st + 1);
+                af[st] = finish_step(sw);
+                if (st + 1 < kSteps) sw = nx;
+            }
+        }
+        lds_barrier();  // every wavefront has read the previous unit's operands
+#pragma unroll
+        for (int st = 0; st < kSteps; ++st) abuf[j][st][lane] = __builtin_bit_cast(uint4, af[st]);
+        lds_barrier();
+        int64_t setn = set, ktn = kt + 1;
+        if (ktn == a.KT) {
+            ktn = 0;
+            ++setn;
+        }
+        const bool more = uu + 1 < u1;
+        const int64_t kx = more ? ktn : kt;  // X of the next unit (past the range's end: this one's, unused)
+        // The X loads are issued whatever the wavefront's tokens or the range:
+        // a path with fewer loads would make the compiler's merged waits drain
+        // the record ring. The A operands of step st + 1 are requested before
+        // step st's products issue (kept there by a scheduling barrier): read
+        // one at a time just before use, their LDS latency set the pace.
+        half8 av[2][R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) av[0][r] = __builtin_bit_cast(half8, abuf[r][0][lane]);
+#pragma unroll
+        for (int st = 0; st < kSteps; ++st) {
+            if (st + 1 < kSteps) {
+#pragma unroll
+                for (int r = 0; r < R; ++r) av[(st + 1) & 1][r] = __builtin_bit_cast(half8, abuf[r][st + 1][lane]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            if (has_tokens) {
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+#pragma unroll
+                    for (int nb = 0; nb < NB; ++nb)
+                        acc[r][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                            av[st & 1][r], __builtin_bit_cast(half8, xb[nb][st]), acc[r][nb], 0, 0, 0);
+            }
+            // This step's X for the next unit, as soon as its last MFMA is issued.
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) xb[nb][st] = __builtin_amdgcn_raw_buffer_load_b128(xr, x_at(kx, st, nb), 0, 0);
+        }
+        if (cnt_set >= 0) {
+            const WaveArgs ac = a;
+            arrive_finish<R, NB>(ac, cnt_set, cnt_nseg, cnt_old, lane, j);
+            cnt_set = -1;
+        }
+        if (pend_set >= 0) {  // the partial stored at the end of the previous unit
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kPartWait) : "memory");
+            cnt_old = arrive_count(a, pend_set, lane, j);
+            cnt_set = pend_set;
+            cnt_nseg = pend_nseg;
+            pend_set = -1;
+        }
+        if (!more || ktn == 0) {  // end of this workgroup's segment of the row set
+            const int64_t w_first = unit_owner(set * a.KT, a.units, G);
+            const int64_t w_last = unit_owner(set * a.KT + a.KT - 1, a.units, G);
+            if (has_tokens) {
+                const WaveArgs ac = a;
+                if (w_first == w_last) {
+#pragma unroll
+                    for (int nb = 0; nb < NB; ++nb) {
+                        const int tok = tok0 + 16 * nb + n_lane;
+                        if (tok < a.N) {
+#pragma unroll
+                            for (int r = 0; r < R; ++r) store_rows4(ac, tok, (set * R + r) * kTileRows + g4, acc[r][nb]);
+                        }
+                    }
+                } else {
+                    const int64_t slot_floats = (int64_t)a.N * kTileRows * R;
+                    float *part_slot = a.ws + (set * a.maxseg + (w - w_first)) * slot_floats;
+                    const __amdgpu_buffer_rsrc_t part = __builtin_amdgcn_make_buffer_rsrc(
+                        part_slot, (short)0, (int)(slot_floats * 4), kBufferRsrcWord3);
+#pragma unroll
+                    for (int nb = 0; nb < NB; ++nb) {
+                        const int tok = tok0 + 16 * nb + n_lane;
+                        if (tok < a.N) {
+#pragma unroll
+                            for (int r = 0; r < R; ++r)
+                                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, acc[r][nb]), part,
+                                                                       (tok * kTileRows * R + kTileRows * r + g4) * 4,
+                                                                       0, kCachePolicyDevice);
+                        }
+                    }
+                    pend_set = set;
+                    pend_nseg = w_last - w_first + 1;
+                }
+            }
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb) acc[r][nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        }
+        dma(slot, onext);  // unit uu + 2, into the slot this unit's decode freed
+        onext = onn;
+        set = setn;
+        kt = ktn;
+    };
+    // Whole rounds of S units, then the rest: no path through the main loop
+    // skips a unit's loads, so the compiler's waits there stay exact.
+    int64_t u = u0;
+    for (; u + S <= u1; u += S) static_for([&](auto pc) { unit(u + pc.value, pc); }, std::make_integer_sequence<int, S>{});
+    static_for(
+        [&](auto pc) {
+            if (pc.value < S - 1 && u + pc.value < u1) unit(u + pc.value, pc);
+        },
+        std::make_integer_sequence<int, S>{});
+    __builtin_amdgcn_s_waitcnt(0);  // the transfers past the range's end, the last partial's stores
+    if (cnt_set >= 0) arrive_finish<R, NB>(a, cnt_set, cnt_nseg, cnt_old, lane, j);
+    if (pend_set >= 0) arrive_row_set<R, NB>(a, pend_set, pend_nseg, lane, j);
+}
+
+// ---------------------------------------------------------------------------
 // Row-block kernel for small matrices (up to 16 tokens).
 //
 // One workgroup per row block: its W wavefronts split the row block's column
@@ -1300,7 +1638,7 @@ static int pass_nt(const usp_matrix *A, int64_t N, int64_t n0) {
 // Plans of the single-pass kernels (up to 128 tokens).
 // ---------------------------------------------------------------------------
 
-enum WaveKind { kWaveNone = 0, kWaveDma4 = 1, kWaveRow = 2, kWaveChunk = 3 };
+enum WaveKind { kWaveNone = 0, kWaveDma4 = 1, kWaveRow = 2, kWaveChunk = 3, kWaveShare = 4 };
 
 constexpr int kMinWaveLoads = 2;  // record load groups instantiated: 2..8
 // The fewest units a direct-to-LDS wavefront streams before a split costs it a
@@ -1441,6 +1779,50 @@ static int resident_waves(int loads, int nb) {
     return cached_occupancy(cached[loads][nb], reinterpret_cast<const void *>(dma_kernel(loads, nb)), kLanes);
 }
 
+static WaveKernelFn share_kernel(int loads, int nb) {
+#define USP_SHARE(NB)                                 \
+    switch (loads) {                                  \
+        case 2: return spmm_share_kernel<2, NB>;      \
+        case 3: return spmm_share_kernel<3, NB>;      \
+        case 4: return spmm_share_kernel<4, NB>;      \
+        case 5: return spmm_share_kernel<5, NB>;      \
+        case 6: return spmm_share_kernel<6, NB>;      \
+        case 7: return spmm_share_kernel<7, NB>;      \
+        default: return spmm_share_kernel<8, NB>;     \
+    }
+    if (nb == 1) {
+        USP_SHARE(1)
+    }
+    if (nb == 2) {
+        USP_SHARE(2)
+    }
+    if (nb == 3) {
+        USP_SHARE(3)
+    }
+    USP_SHARE(4)
+#undef USP_SHARE
+}
+
+// Workgroups of the shared-decode kernel resident per CU.
+static int resident_share_wgs(int loads, int nb) {
+    static std::atomic<int> cached[9][kMaxDmaTokenBlocks + 1];
+    return cached_occupancy(cached[loads][nb], reinterpret_cast<const void *>(share_kernel(loads, nb)),
+                            kShareWaves * kLanes);
+}
+
+// Token blocks per wavefront of the shared-decode kernel (its four wavefronts
+// split the tokens).
+static int share_nb(int64_t N) { return (int)ceil_div(ceil_div(N, 16), kShareWaves); }
+
+// The fewest units a shared-decode workgroup streams.
+constexpr int64_t kMinUnitsPerShareWg = 4;
+// Token blocks from which the shared-decode kernel serves a call (measured,
+// packed X included): 70B FFN 84.2 against 89.4 us on the direct-to-LDS kernel
+// at 48 tokens, 87.3 against 104.9 at 64; 13B FFN up 37.2 against 37.7 on the
+// four-wavefront kernel at 48, 38.7 against 41.4 at 64. At 32 tokens two of
+// its four wavefronts would have no tokens.
+constexpr int kShareMinBlocks = 3;
+
 struct WavePlan {
     WaveKind kind;
     int loads, rows, nb, tg;  // record load groups; row blocks per unit; token blocks per wavefront; groups
@@ -1466,6 +1848,19 @@ constexpr int64_t kChunkMaxTiles = 20480;
 constexpr int64_t kChunkMaxSplit = 8;
 static WaveKind wave_kind(const usp_matrix *A, int loads, int64_t N) {
     const int nb = (int)ceil_div(N, 16);
+    // More than 32 tokens: the shared-decode kernel (each record decoded once,
+    // X packed) on matrices with at least kMinUnitsPerShareWg units for every
+    // resident workgroup, and above 64 tokens for one workgroup per CU. Between
+    // the two, at 33-64 tokens, the kernels are within 7% either way: 13B
+    // attention (1600 units) 21.4 us on the four-wavefront kernel against 22.9
+    // at 48 tokens, 24.0 against 25.2 at 64; one GPU's share of the 70B FFN
+    // (1792 units) 26.0 against 24.8 and 29.8 against 28.1. At 128 tokens 13B
+    // attention takes 36.6 us on the shared-decode kernel against 40.9.
+    if (nb >= kShareMinBlocks && nb <= kMaxDmaTokenBlocks * kShareWaves && dma_loads(A, 1) <= kMaxWaveLoads) {
+        const int64_t cus = A->num_cus > 0 ? A->num_cus : 256;
+        const int64_t per = nb > kShareWaves ? 1 : resident_share_wgs(dma_loads(A, 1), share_nb(N));
+        if (ceil_div(A->RB, kShareWaves) * A->KT >= kMinUnitsPerShareWg * cus * per) return kWaveShare;
+    }
     if (nb <= kMaxDmaTokenBlocks * kMaxDmaTokenGroups) {
         int nbw, tg;
         dma_tokens(N, nbw, tg);
@@ -1528,6 +1923,22 @@ static WavePlan plan_wave(const usp_matrix *A, int64_t N) {
         p.split = p.maxseg > 1;
         return p;
     }
+    if (p.kind == kWaveShare) {
+        p.nb = share_nb(N);
+        p.tg = kShareWaves;  // one arrival counter per wavefront (token slice)
+        p.loads = dma_loads(A, 1);
+        p.rows = kShareWaves;
+        p.sets = ceil_div(A->RB, p.rows);
+        p.units = p.sets * A->KT;
+        const int64_t wgs = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_share_wgs(p.loads, p.nb);
+        const int64_t want = ceil_div(p.units, kMinUnitsPerShareWg);
+        p.ranges = want < wgs ? want : wgs;
+        p.grid = p.ranges;
+        const int64_t shortest = p.units / p.ranges;
+        p.maxseg = ceil_div(A->KT, shortest) + 1;
+        p.split = (p.units % p.ranges != 0) || ((p.units / p.ranges) % A->KT != 0);
+        return p;
+    }
     p.nb = 1;
     p.tg = 1;
     if (p.kind != kWaveDma4) {  // the row-block kernel (or none): no partials in the workspace
@@ -1560,7 +1971,8 @@ constexpr int64_t kMaxWaveTokens = 16 * kMaxDmaTokenBlocks * kMaxDmaTokenGroups;
 static bool use_wave_kernel(const usp_matrix *A, const void *X, int64_t ldx, int64_t N) {
     if (N > kMaxWaveTokens || (reinterpret_cast<uintptr_t>(X) & 15) || ldx % 8 || A->K % 8) return false;
     const int64_t x_bytes = ((N - 1) * ldx + A->K) * 2;
-    if (x_bytes + 2 * A->KT * kTileK >= ((int64_t)1 << 31) || (A->RB * A->KT + 1) * 4 >= ((int64_t)1 << 31))
+    if (x_bytes + 2 * A->KT * kTileK >= ((int64_t)1 << 31) || (A->RB * A->KT + 1) * 4 >= ((int64_t)1 << 31) ||
+        packed_x_bytes(A->KT, N) + 16 * kPackBlockBytes >= ((size_t)1 << 31))
         return false;
     return wave_kind(A, wave_loads(A), N) != kWaveNone;
 }
@@ -1580,6 +1992,8 @@ std::string describe_plan(const usp_matrix *A, int64_t N) {
             if (kind == kWaveChunk)
                 snprintf(buf, sizeof buf, "chunk S=%lld W=%d nb=%d grid=%lld", (long long)p.maxseg, p.wpg, p.nb,
                          (long long)p.grid);
+            else if (kind == kWaveShare)
+                snprintf(buf, sizeof buf, "share nb=%d grid=%lld", p.nb, (long long)p.grid);
             else
                 snprintf(buf, sizeof buf, "dma nb=%d tg=%d grid=%lld", p.nb, p.tg, (long long)p.grid);
         }
@@ -1615,12 +2029,22 @@ static size_t wave_partials_bytes(const usp_matrix *A, int64_t N) {
     return (size_t)p.sets * (size_t)p.maxseg * (size_t)N * kTileRows * p.rows * sizeof(float);
 }
 
+// Where the shared-decode kernel's packed X starts: after the counters and
+// the partials (256-byte aligned).
+static size_t packed_x_offset(const usp_matrix *A, int64_t N) {
+    return counters_bytes(A) + (wave_partials_bytes(A, N) + 255) / 256 * 256;
+}
+
 size_t spmm_workspace_bytes(const usp_matrix *A, int64_t N) {
     // Layout: counters, then the partials of whichever pass runs. Passes run one
     // after another and reuse the workspace: full passes of pass_tokens(A)
-    // tokens, then one pass over the remainder; up to 128 tokens may take a wave
-    // kernel (sized here too, whichever needs more).
+    // tokens, then one pass over the remainder; up to 256 tokens may take a wave
+    // kernel (sized here too, whichever needs more; a call whose X the wave
+    // kernels cannot read goes to the passes). The shared-decode kernel also
+    // keeps packed X after its partials.
     size_t need = N <= kMaxWaveTokens ? wave_partials_bytes(A, N) : 0;
+    if (N <= kMaxWaveTokens && wave_kind(A, wave_loads(A), N) == kWaveShare)
+        need = packed_x_offset(A, N) - counters_bytes(A) + packed_x_bytes(A->KT, N);
     auto add = [&](int64_t nb) {
         const SpmmPlan p = plan_pass(A, (int)((nb + 15) / 16));
         if (p.split) need = std::max(need, partials_bytes(p, nb));
@@ -1664,7 +2088,7 @@ static int launch_wave(const usp_matrix *A, const void *X, int64_t ldx, void *Y,
                        const Epilogue &ep, void *workspace, hipStream_t st) {
     if (wave_kind(A, wave_loads(A), N) == kWaveRow) return launch_row(A, X, ldx, Y, ldy, N, ep, st);
     const WavePlan p = plan_wave(A, N);
-    WaveArgs a;
+    WaveArgs a = {};
     a.M = A->M;
     a.K = A->K;
     a.RB = A->RB;
@@ -1686,6 +2110,16 @@ static int launch_wave(const usp_matrix *A, const void *X, int64_t ldx, void *Y,
     if (p.kind == kWaveChunk)
         hipLaunchKernelGGL(chunk_kernel(p.loads, p.wpg, p.nb), dim3((unsigned)p.grid), dim3(kLanes * p.wpg), 0, st, a,
                            A->d_off, reinterpret_cast<const uint8_t *>(A->d_stream));
+    else if (p.kind == kWaveShare) {
+        uint8_t *xp = reinterpret_cast<uint8_t *>(workspace) + packed_x_offset(A, N);
+        a.tb = (int)ceil_div(N, 16);
+        a.xp = xp;
+        a.xp_bytes = (uint32_t)packed_x_bytes(A->KT, N);
+        hipLaunchKernelGGL(pack_x_kernel, dim3((unsigned)(A->KT * a.tb)), dim3(kLanes), 0, st,
+                           reinterpret_cast<const uint16_t *>(X), ldx, (int)N, A->K, a.tb, xp);
+        hipLaunchKernelGGL(share_kernel(p.loads, p.nb), dim3((unsigned)p.grid), dim3(kShareWaves * kLanes), 0, st, a,
+                           A->d_off, reinterpret_cast<const uint8_t *>(A->d_stream));
+    }
     else
         hipLaunchKernelGGL(dma_kernel(p.loads, p.nb), dim3((unsigned)p.grid), dim3(kLanes), 0, st, a, A->d_off,
                            reinterpret_cast<const uint8_t *>(A->d_stream));

@@ -277,25 +277,42 @@ def test_dma_kernel_two_token_blocks_ragged(torch, usp):
     assert_close(Y, W, mask, X)
 
 
-# Three and four token blocks per wavefront of the direct-to-LDS kernel (X
-# double-buffered, all 8 steps' LDS reads issued first), and above 64 tokens
-# its token groups (wavefronts streaming the same units, each for its own
-# blocks). Exact on small integers at 48 (3 blocks), 64 (4), 128 (2 groups of
-# 4) and 176 tokens (groups of 4, 4 and 3); tolerance at 40, 100 (2 groups of
-# 4, the last block partly past N) and 250 tokens (4 groups of 4).
-@pytest.mark.parametrize("N", [48, 64, 128, 176])
-def test_dma_kernel_token_groups_exact(torch, usp, N):
+# The shared-decode kernel (33 to 256 tokens on large layers: four
+# wavefronts decode one record each into LDS, each multiplies all four by its
+# quarter of the tokens, X packed in product order first). Exact on small
+# integers, every output, at 48 and 64 tokens (one block per wavefront, the
+# last wavefronts partly or wholly without tokens), 128 (two), 176 (three, the
+# last wavefront's third block empty) and 256 (four); tolerance at 40, 100
+# and 250 tokens. M = 36880 leaves the last set of 4 row blocks one block
+# short, K = 8088 ends in a partial column tile (zeros in the packed X).
+@pytest.mark.parametrize("N", [48, 64, 128, 176, 256])
+def test_share_kernel_exact(torch, usp, N):
     W, mask, X = wl.make_small_int(36880, 8088, N, 0.5, seed=27 + N, lo=-1, hi=1)
+    A = usp.SparseMatrix(W, mask)
+    plan = A.plan(N)
+    A.free()
+    print(f"case N={N}: {plan}", flush=True)
+    assert plan.startswith("share"), plan
     Y = run(torch, usp, W, mask, X)
     Yref, _ = oracle.masked_gemm(W, mask, X)
     assert np.array_equal(Y, Yref)
 
 
 @pytest.mark.parametrize("N", [40, 100, 250])
-def test_dma_kernel_token_groups_ragged(torch, usp, N):
+def test_share_kernel_ragged(torch, usp, N):
     W, mask, X = wl.make_random(36880, 8088, N, 0.5, seed=28 + N)
     Y = run(torch, usp, W, mask, X)
     assert_close(Y, W, mask, X)
+
+
+# A call the wave kernels cannot take (X not 16-byte aligned, ldx odd) on a
+# shape that the shared-decode kernel serves otherwise: the passes of the
+# four-wavefront kernel run in the workspace sized for both routes.
+def test_share_shape_unaligned_x_passes(torch, usp):
+    W, mask, X = wl.make_small_int(36880, 8088, 64, 0.5, seed=29, lo=-1, hi=1)
+    Y = run(torch, usp, W, mask, X, ldx_extra=3, offset=1)
+    Yref, _ = oracle.masked_gemm(W, mask, X)
+    assert np.array_equal(Y, Yref)
 
 
 # 33 to 64 tokens on a matrix whose last row group has one real row block (257
@@ -548,7 +565,8 @@ def test_chunk_kernel_short_last_chunk_exact(torch, usp, M, K, N):
 # products must leave their arrival counters at zero for the next replay. Every
 # kernel: row-block (1024 x 1024, 16), column-chunk (5120 x 5120, 16 and, with
 # two token blocks, 32; 5 chunks per row block), direct-to-LDS (36880 x 8088 at
-# 16 and 100 tokens), and four-wavefront (4101 x 1000, 48).
+# 16 tokens), shared-decode (36880 x 8088 at 100 tokens: the X-packing kernel,
+# then the product) and four-wavefront (4101 x 1000, 48).
 @pytest.mark.parametrize("M,K,N", [(1024, 1024, 16), (5120, 5120, 16), (5120, 5120, 32), (36880, 8088, 16),
                                    (36880, 8088, 100), (4101, 1000, 48)])
 def test_graph_capture_replays(torch, usp, M, K, N):
@@ -586,9 +604,10 @@ def test_graph_capture_replays(torch, usp, M, K, N):
 # column-chunk kernel for small layers at 9-16 tokens unless a row block would
 # split into more than 8 chunks, and at 17-32 tokens when one round of its
 # workgroups of 8 row blocks covers at least half the CUs; the direct-to-LDS
-# kernel for large layers up to 256 tokens (token groups above 64; at 3-4
-# blocks only if no row set splits over more than 4 wavefronts); the
-# four-wavefront kernel otherwise, in passes above 256 tokens. The route depends only on the shape, the token count and
+# kernel for large layers up to 32 tokens; the shared-decode kernel from 33 to
+# 256 tokens on layers with at least 4 units of 4 row blocks per CU (the 70B
+# FFN down projection, 13B attention at 128); the four-wavefront kernel
+# otherwise, in passes above 256 tokens. The route depends only on the shape, the token count and
 # the largest record, so a 50% Bernoulli mask over constant weights stands in.
 # The column-chunk kernel takes 8 row blocks per workgroup when all its
 # workgroups are resident at once, else 4.
@@ -600,10 +619,10 @@ ROUTES = [
     ((13824, 5120, 32), "fourwave passes=1 nt=2"), ((1024, 1024, 32), "fourwave passes=1 nt=2"),
     ((5120, 13824, 16), "fourwave passes=1 nt=1"),
     ((4101, 1000, 48), "fourwave passes=1 nt=3"), ((4101, 1000, 200), "fourwave passes=2 nt=8"),
-    ((8192, 28672, 64), "fourwave passes=1 nt=4"), ((36880, 8088, 300), "fourwave passes=5 nt=4"),
+    ((8192, 28672, 64), "share nb=1"), ((36880, 8088, 300), "fourwave passes=5 nt=4"),
     ((36880, 8088, 16), "dma nb=1 tg=1"), ((36880, 8088, 32), "dma nb=2 tg=1"),
-    ((36880, 8088, 64), "dma nb=4 tg=1"), ((36880, 8088, 100), "dma nb=4 tg=2"),
-    ((8192, 28672, 128), "dma nb=4 tg=2"),
+    ((36880, 8088, 48), "share nb=1"), ((36880, 8088, 64), "share nb=1"), ((36880, 8088, 100), "share nb=2"),
+    ((8192, 28672, 128), "share nb=2"), ((28672, 8192, 256), "share nb=4"), ((5120, 5120, 128), "share nb=2"),
 ]
 
 

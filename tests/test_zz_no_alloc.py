@@ -18,13 +18,15 @@ def test_noalloc_matches_spmm_two_calls():
     assert torch.cuda.is_available()
     lib = usp.load_library()
     # First a split product (partials and arrival counters in the scratch), then a smaller one
-    # through another kernel, then the first again: each equals usp_spmm bit for bit.
+    # through another kernel, then the four-wavefront and the shared-decode kernels (the latter
+    # with packed X in the scratch too), then the first again: each equals usp_spmm bit for bit.
     cases = [wl.make_random(5120, 5120, 16, 0.5, seed=601), wl.make_random(1024, 1024, 8, 0.5, seed=602),
-             wl.make_random(4101, 1000, 48, 0.5, seed=603)]
+             wl.make_random(4101, 1000, 48, 0.5, seed=603), wl.make_random(5120, 5120, 128, 0.5, seed=605)]
     for i, (W, mask, X) in enumerate(cases + cases[:1]):
         print(f"case {i}: M={W.shape[0]} K={W.shape[1]} N={X.shape[0]}", flush=True)
         A = usp.SparseMatrix(W, mask)
         need = A.workspace_size(X.shape[0])
+        print(f"  {A.plan(X.shape[0])}, workspace {need} bytes", flush=True)
         assert need <= usp.NOALLOC_SCRATCH_BYTES, need
         Xd = torch.from_numpy(X.view(np.float16)).cuda()
         Yn = torch.full((X.shape[0], A.M), float("nan"), dtype=torch.float16, device="cuda")
