@@ -1446,6 +1446,228 @@ __global__ __launch_bounds__(kShareWaves *kLanes, NB <= 2 ? 2 : 1) void spmm_sha
     if (pend_set >= 0) arrive_row_set<R, NB>(a, pend_set, pend_nseg, lane, j);
 }
 
+// The shared-decode kernel with the decode of unit u + 1 interleaved with the
+// products of unit u. With 3-4 token blocks a wavefront needs more than 256
+// registers, so each SIMD holds one wavefront and the kernel above alternates a
+// decode (VALU and LDS) with the products (MFMA), overlapping neither. Here the
+// A operands are double-buffered in LDS: in each step of unit u a wavefront
+// issues that step's products from buffer u mod 2 and decodes the same step of
+// its record of unit u + 1 into the other buffer, and one barrier per unit
+// (instead of two) both publishes the new buffer and frees the old one. The
+// record of unit u + 1 must be in its ring slot when unit u starts; the
+// transfer of unit v + 2 goes into the slot freed by decoding unit v, at the end
+// of unit v - 1 (two units of slack). LDS: two 2-slot rings, two 32 KB operand
+// buffers (105 KB at 5 KB records): one workgroup per CU.
+template <int L, int NB>
+__global__ __launch_bounds__(kShareWaves *kLanes, 1) void spmm_pipe_kernel(WaveArgs a, const uint32_t *__restrict__ off,
+                                                                          const uint8_t *__restrict__ stream) {
+    constexpr int R = kShareWaves;
+    constexpr int kSlot = 1024 * L + 16;
+    __shared__ __attribute__((aligned(16))) uint8_t ring0[R][kSlot];
+    __shared__ __attribute__((aligned(16))) uint8_t ring1[R][kSlot];
+    __shared__ __attribute__((aligned(16))) uint4 abuf0[R][kSteps][kLanes];
+    __shared__ __attribute__((aligned(16))) uint4 abuf1[R][kSteps][kLanes];
+    __shared__ __attribute__((aligned(16))) uint8_t lut[16 * 8];
+    uint8_t *const ring[2] = {ring0[0], ring1[0]};
+    const int lane = threadIdx.x & (kLanes - 1);
+    const int j = __builtin_amdgcn_readfirstlane(threadIdx.x / kLanes);
+    const int64_t w = blockIdx.x, G = gridDim.x;
+    const int64_t u0 = w * a.units / G, u1 = (w + 1) * a.units / G;
+    if (u0 >= u1) return;  // the whole workgroup
+    if (threadIdx.x < 16) reinterpret_cast<uint2 *>(lut)[threadIdx.x] = nibble_selectors((uint32_t)threadIdx.x);
+
+    const __amdgpu_buffer_rsrc_t xr =
+        __builtin_amdgcn_make_buffer_rsrc((void *)a.xp, (short)0, (int)a.xp_bytes, kBufferRsrcWord3);
+    const __amdgpu_buffer_rsrc_t offr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)off, (short)0, (int)((a.RB * a.KT + 1) * 4), kBufferRsrcWord3);
+    const int n_lane = lane & 15, g4 = 4 * (lane >> 4);
+    const int tok0 = 16 * NB * j;
+    const bool has_tokens = tok0 < a.N;
+    const int xlane = (NB * j * 64 + lane) * 16;
+    auto x_at = [&](int64_t kx, int st, int nb) -> int {
+        return (int)((kx * kSteps + st) * a.tb + nb) * (int)kPackBlockBytes + xlane;
+    };
+    auto rec_offsets = [&](int64_t set, int64_t kt, bool real) -> uint32_t {
+        const int64_t rb = set * R + j;
+        const bool ok = real && lane < 2 && rb < a.RB;
+        return __builtin_amdgcn_raw_buffer_load_b32(offr, ok ? (int)((rb * a.KT + kt + lane) * 4) : 0x7FFFFFF0, 0, 0);
+    };
+    auto advance = [&](int64_t &set, int64_t &kt) {
+        if (++kt == a.KT) {
+            kt = 0;
+            ++set;
+        }
+    };
+    auto dma = [&](uint8_t *slot, uint32_t o) {
+        const uint32_t lds = (uint32_t)reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint8_t *)slot);
+        dma_rec_asm<L>(stream, __builtin_amdgcn_readlane(o, 0), __builtin_amdgcn_readlane(o, 1), lane, lds);
+    };
+    // Decodes this wavefront's record in `slot` straight into row block j of
+    // the operand buffer `dst` (the prologue's whole-record decode).
+    auto decode_to = [&](const uint8_t *slot, uint4 (*dst)[kSteps][kLanes]) {
+        const RecState rs = rec_state(slot_mask(slot, lane));
+        lds_u32 *const vals = as_lds(slot + kMaskBytes);
+        StepWords sw = read_step(vals, lut, rs, 0);
+#pragma unroll
+        for (int st = 0; st < kSteps; ++st) {
+            StepWords nx;
+            if (st + 1 < kSteps) nx = read_step(vals, lut, rs, st + 1);
+            dst[j][st][lane] = __builtin_bit_cast(uint4, finish_step(sw));
+            if (st + 1 < kSteps) sw = nx;
+        }
+    };
+    // Vector memory instructions issued after the transfer of the record a
+    // unit decodes (that of the next unit) and before that decode, on the path
+    // with the fewest: the transfer is issued at the end of the unit two before;
+    // then the previous unit's offset load (1), its X loads (kSteps NB) and its
+    // transfer (L), and this unit's offset load (1). One fewer is waited for.
+    // The first unit's record (the prologue's second transfer) is followed by
+    // X (kSteps NB), the third transfer (L) and the offset load (1): the same.
+    constexpr int kRecWait = kSteps * NB + L + 1 < 63 ? kSteps * NB + L + 1 : 63;
+    // The prologue decodes the first record once X and the second transfer
+    // follow it: kSteps NB + L instructions.
+    constexpr int kFirstWait = kSteps * NB + L < 63 ? kSteps * NB + L : 63;
+    constexpr int kPartWait = kSteps * NB + L + 1 < 63 ? kSteps * NB + L + 1 : 63;
+
+    floatx4 acc[R][NB];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[r][nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    int64_t set = u0 / a.KT, kt = u0 % a.KT;
+    int64_t la_set = set, la_kt = kt;
+    const uint32_t oa = rec_offsets(la_set, la_kt, true);
+    advance(la_set, la_kt);
+    const uint32_t ob = rec_offsets(la_set, la_kt, u0 + 1 < u1);
+    advance(la_set, la_kt);
+    const uint32_t oc = rec_offsets(la_set, la_kt, u0 + 2 < u1);
+    advance(la_set, la_kt);
+    uint32_t onext = rec_offsets(la_set, la_kt, u0 + 3 < u1);  // requested at the end of the first unit
+    advance(la_set, la_kt);
+    dma(ring[0] + j * kSlot, oa);
+    dma(ring[1] + j * kSlot, ob);
+    v4u32 xb[NB][kSteps];
+#pragma unroll
+    for (int st = 0; st < kSteps; ++st)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) xb[nb][st] = __builtin_amdgcn_raw_buffer_load_b128(xr, x_at(kt, st, nb), 0, 0);
+    lds_barrier();  // the selector table
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kFirstWait) : "memory");
+    decode_to(ring[0] + j * kSlot, abuf0);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    dma(ring[0] + j * kSlot, oc);  // unit u0 + 2 into the slot just decoded
+    lds_barrier();                 // the first unit's operands
+
+    int64_t pend_set = -1, pend_nseg = 0;
+    int64_t cnt_set = -1, cnt_nseg = 0;
+    uint32_t cnt_old = 0;
+    // One unit: par = (uu - u0) mod 2 selects its operand buffer (the next
+    // unit's record sits in ring slot 1 - par).
+    auto unit = [&](int64_t uu, auto parc) __attribute__((always_inline)) {
+        constexpr int par = decltype(parc)::value;
+        uint4 (*const acur)[kSteps][kLanes] = par ? abuf1 : abuf0;
+        uint4 (*const anext)[kSteps][kLanes] = par ? abuf0 : abuf1;
+        uint8_t *const slot = ring[1 - par] + j * kSlot;  // the next unit's record
+        const uint32_t onn = rec_offsets(la_set, la_kt, uu + 4 < u1);
+        advance(la_set, la_kt);
+        int64_t setn = set, ktn = kt + 1;
+        if (ktn == a.KT) {
+            ktn = 0;
+            ++setn;
+        }
+        const bool more = uu + 1 < u1;
+        const int64_t kx = more ? ktn : kt;
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kRecWait) : "memory");
+        const RecState rs = rec_state(slot_mask(slot, lane));
+        lds_u32 *const vals = as_lds(slot + kMaskBytes);
+        // The products are issued whether or not this wavefront has tokens
+        // (without tokens its results are never stored): a branch around them
+        // would keep the scheduler from interleaving them with the decode.
+        StepWords sw = read_step(vals, lut, rs, 0);
+#pragma unroll
+        for (int st = 0; st < kSteps; ++st) {
+            StepWords nx;
+            if (st + 1 < kSteps) nx = read_step(vals, lut, rs, st + 1);
+            half8 av[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r) av[r] = __builtin_bit_cast(half8, acur[r][st][lane]);
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb)
+                    acc[r][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[r], __builtin_bit_cast(half8, xb[nb][st]),
+                                                                      acc[r][nb], 0, 0, 0);
+            anext[j][st][lane] = __builtin_bit_cast(uint4, finish_step(sw));
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) xb[nb][st] = __builtin_amdgcn_raw_buffer_load_b128(xr, x_at(kx, st, nb), 0, 0);
+            if (st + 1 < kSteps) sw = nx;
+        }
+        if (cnt_set >= 0) {
+            const WaveArgs ac = a;
+            arrive_finish<R, NB>(ac, cnt_set, cnt_nseg, cnt_old, lane, j);
+            cnt_set = -1;
+        }
+        if (pend_set >= 0) {
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kPartWait) : "memory");
+            cnt_old = arrive_count(a, pend_set, lane, j);
+            cnt_set = pend_set;
+            cnt_nseg = pend_nseg;
+            pend_set = -1;
+        }
+        if (!more || ktn == 0) {
+            const int64_t w_first = unit_owner(set * a.KT, a.units, G);
+            const int64_t w_last = unit_owner(set * a.KT + a.KT - 1, a.units, G);
+            if (has_tokens) {
+                const WaveArgs ac = a;
+                if (w_first == w_last) {
+#pragma unroll
+                    for (int nb = 0; nb < NB; ++nb) {
+                        const int tok = tok0 + 16 * nb + n_lane;
+                        if (tok < a.N) {
+#pragma unroll
+                            for (int r = 0; r < R; ++r) store_rows4(ac, tok, (set * R + r) * kTileRows + g4, acc[r][nb]);
+                        }
+                    }
+                } else {
+                    const int64_t slot_floats = (int64_t)a.N * kTileRows * R;
+                    float *part_slot = a.ws + (set * a.maxseg + (w - w_first)) * slot_floats;
+                    const __amdgpu_buffer_rsrc_t part = __builtin_amdgcn_make_buffer_rsrc(
+                        part_slot, (short)0, (int)(slot_floats * 4), kBufferRsrcWord3);
+#pragma unroll
+                    for (int nb = 0; nb < NB; ++nb) {
+                        const int tok = tok0 + 16 * nb + n_lane;
+                        if (tok < a.N) {
+#pragma unroll
+                            for (int r = 0; r < R; ++r)
+                                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, acc[r][nb]), part,
+                                                                       (tok * kTileRows * R + kTileRows * r + g4) * 4,
+                                                                       0, kCachePolicyDevice);
+                        }
+                    }
+                    pend_set = set;
+                    pend_nseg = w_last - w_first + 1;
+                }
+            }
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb) acc[r][nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the decode's reads of the slot are done
+        dma(slot, onext);  // unit uu + 3, into the slot just decoded
+        onext = onn;
+        set = setn;
+        kt = ktn;
+        lds_barrier();  // the next unit's operands are complete, this unit's free
+    };
+    int64_t u = u0;
+    for (; u + 2 <= u1; u += 2) static_for([&](auto pc) { unit(u + pc.value, pc); }, std::make_integer_sequence<int, 2>{});
+    if (u < u1) unit(u, std::integral_constant<int, 0>{});
+    __builtin_amdgcn_s_waitcnt(0);
+    if (cnt_set >= 0) arrive_finish<R, NB>(a, cnt_set, cnt_nseg, cnt_old, lane, j);
+    if (pend_set >= 0) arrive_row_set<R, NB>(a, pend_set, pend_nseg, lane, j);
+}
+
 // ---------------------------------------------------------------------------
 // Row-block kernel for small matrices (up to 16 tokens).
 //
@@ -1803,8 +2025,49 @@ static WaveKernelFn share_kernel(int loads, int nb) {
 #undef USP_SHARE
 }
 
-// Workgroups of the shared-decode kernel resident per CU.
-static int resident_share_wgs(int loads, int nb) {
+static WaveKernelFn pipe_kernel(int loads, int nb) {
+#define USP_PIPE(NB)                                  \
+    switch (loads) {                                  \
+        case 2: return spmm_pipe_kernel<2, NB>;       \
+        case 3: return spmm_pipe_kernel<3, NB>;       \
+        case 4: return spmm_pipe_kernel<4, NB>;       \
+        case 5: return spmm_pipe_kernel<5, NB>;       \
+        case 6: return spmm_pipe_kernel<6, NB>;       \
+        case 7: return spmm_pipe_kernel<7, NB>;       \
+        default: return spmm_pipe_kernel<8, NB>;      \
+    }
+    if (nb == 2) {
+        USP_PIPE(2)
+    }
+    if (nb == 3) {
+        USP_PIPE(3)
+    }
+    USP_PIPE(4)
+#undef USP_PIPE
+}
+
+// Whether the shared-decode kernel overlaps the next unit's decode with the
+// products (spmm_pipe_kernel, one workgroup per CU) for `units` units: always
+// at 3-4 token blocks per wavefront, where either way a SIMD holds one
+// wavefront (70B FFN at 256 tokens 174.5 against 191.4 us, 66B FFN 241.7
+// against 265.8, 13B FFN up 68.7 against 71.9); at 2 blocks only on layers of
+// fewer than 32 units per CU, where two unpipelined workgroups per CU have too
+// few units to hide each other (13B attention at 128 tokens 32.4 against 36.6,
+// 13B FFN down 55.1 against 58.8; the 70B FFN, 56 units per CU, 131.8 against
+// 109.5).
+constexpr int kPipeMinBlocks = 3;
+constexpr int64_t kPipeMaxUnitsPerCuAt2 = 32;
+static bool share_pipelined(int nb, int64_t units, int64_t cus) {
+    return nb >= kPipeMinBlocks || (nb == 2 && units < kPipeMaxUnitsPerCuAt2 * cus);
+}
+
+// Workgroups of the shared-decode kernel (pipelined or not) resident per CU.
+static int resident_share_wgs(int loads, int nb, bool pipe = false) {
+    if (pipe) {
+        static std::atomic<int> cached_pipe[9][kMaxDmaTokenBlocks + 1];
+        return cached_occupancy(cached_pipe[loads][nb], reinterpret_cast<const void *>(pipe_kernel(loads, nb)),
+                                kShareWaves * kLanes);
+    }
     static std::atomic<int> cached[9][kMaxDmaTokenBlocks + 1];
     return cached_occupancy(cached[loads][nb], reinterpret_cast<const void *>(share_kernel(loads, nb)),
                             kShareWaves * kLanes);
@@ -1829,6 +2092,7 @@ struct WavePlan {
     int wpg;                  // column-chunk kernel: wavefronts (row blocks) per workgroup
     int64_t sets, units, ranges, grid, maxseg;  // ranges of units; workgroups = ranges * tg
     bool split;
+    bool pipe = false;        // shared-decode kernel: the pipelined variant
 };
 
 // Which kernel suits A for N tokens (measured on MI355X): the direct-to-LDS
@@ -1930,7 +2194,9 @@ static WavePlan plan_wave(const usp_matrix *A, int64_t N) {
         p.rows = kShareWaves;
         p.sets = ceil_div(A->RB, p.rows);
         p.units = p.sets * A->KT;
-        const int64_t wgs = (int64_t)(A->num_cus > 0 ? A->num_cus : 256) * resident_share_wgs(p.loads, p.nb);
+        const int64_t cus = A->num_cus > 0 ? A->num_cus : 256;
+        p.pipe = share_pipelined(p.nb, p.units, cus);
+        const int64_t wgs = cus * resident_share_wgs(p.loads, p.nb, p.pipe);
         const int64_t want = ceil_div(p.units, kMinUnitsPerShareWg);
         p.ranges = want < wgs ? want : wgs;
         p.grid = p.ranges;
@@ -1993,7 +2259,8 @@ std::string describe_plan(const usp_matrix *A, int64_t N) {
                 snprintf(buf, sizeof buf, "chunk S=%lld W=%d nb=%d grid=%lld", (long long)p.maxseg, p.wpg, p.nb,
                          (long long)p.grid);
             else if (kind == kWaveShare)
-                snprintf(buf, sizeof buf, "share nb=%d grid=%lld", p.nb, (long long)p.grid);
+                snprintf(buf, sizeof buf, "share nb=%d grid=%lld%s", p.nb, (long long)p.grid,
+                         p.pipe ? " pipelined" : "");
             else
                 snprintf(buf, sizeof buf, "dma nb=%d tg=%d grid=%lld", p.nb, p.tg, (long long)p.grid);
         }
@@ -2117,8 +2384,9 @@ static int launch_wave(const usp_matrix *A, const void *X, int64_t ldx, void *Y,
         a.xp_bytes = (uint32_t)packed_x_bytes(A->KT, N);
         hipLaunchKernelGGL(pack_x_kernel, dim3((unsigned)(A->KT * a.tb)), dim3(kLanes), 0, st,
                            reinterpret_cast<const uint16_t *>(X), ldx, (int)N, A->K, a.tb, xp);
-        hipLaunchKernelGGL(share_kernel(p.loads, p.nb), dim3((unsigned)p.grid), dim3(kShareWaves * kLanes), 0, st, a,
-                           A->d_off, reinterpret_cast<const uint8_t *>(A->d_stream));
+        hipLaunchKernelGGL(p.pipe ? pipe_kernel(p.loads, p.nb) : share_kernel(p.loads, p.nb),
+                           dim3((unsigned)p.grid), dim3(kShareWaves * kLanes), 0, st, a, A->d_off,
+                           reinterpret_cast<const uint8_t *>(A->d_stream));
     }
     else
         hipLaunchKernelGGL(dma_kernel(p.loads, p.nb), dim3((unsigned)p.grid), dim3(kLanes), 0, st, a, A->d_off,

@@ -282,8 +282,9 @@ def test_dma_kernel_two_token_blocks_ragged(torch, usp):
 # quarter of the tokens, X packed in product order first). Exact on small
 # integers, every output, at 48 and 64 tokens (one block per wavefront, the
 # last wavefronts partly or wholly without tokens), 128 (two), 176 (three, the
-# last wavefront's third block empty) and 256 (four); tolerance at 40, 100
-# and 250 tokens. M = 36880 leaves the last set of 4 row blocks one block
+# last wavefront's third block empty) and 256 (four; at three and four the
+# pipelined variant, which decodes the next unit while multiplying this one);
+# tolerance at 40, 100 and 250 tokens. M = 36880 leaves the last set of 4 row blocks one block
 # short, K = 8088 ends in a partial column tile (zeros in the packed X).
 @pytest.mark.parametrize("N", [48, 64, 128, 176, 256])
 def test_share_kernel_exact(torch, usp, N):
@@ -293,9 +294,33 @@ def test_share_kernel_exact(torch, usp, N):
     A.free()
     print(f"case N={N}: {plan}", flush=True)
     assert plan.startswith("share"), plan
+    assert ("pipelined" in plan) == (N > 128), plan  # 3-4 blocks per wavefront
     Y = run(torch, usp, W, mask, X)
     Yref, _ = oracle.masked_gemm(W, mask, X)
     assert np.array_equal(Y, Yref)
+
+
+# The pipelined variant at two blocks per wavefront, which the planner takes
+# on layers of fewer than 32 units per CU (5120 x 5120: 1600 units): exact at
+# 128 tokens, tolerance at 100 (the last wavefront's second block partly past
+# N).
+@pytest.mark.parametrize("N,exact", [(128, True), (100, False)])
+def test_share_kernel_pipelined_two_blocks(torch, usp, N, exact):
+    if exact:
+        W, mask, X = wl.make_small_int(5120, 5120, N, 0.5, seed=31, lo=-1, hi=1)
+    else:
+        W, mask, X = wl.make_random(5120, 5120, N, 0.5, seed=32)
+    A = usp.SparseMatrix(W, mask)
+    plan = A.plan(N)
+    A.free()
+    print(f"case N={N}: {plan}", flush=True)
+    assert plan.startswith("share nb=2") and "pipelined" in plan, plan
+    Y = run(torch, usp, W, mask, X)
+    if exact:
+        Yref, _ = oracle.masked_gemm(W, mask, X)
+        assert np.array_equal(Y, Yref)
+    else:
+        assert_close(Y, W, mask, X)
 
 
 @pytest.mark.parametrize("N", [40, 100, 250])
