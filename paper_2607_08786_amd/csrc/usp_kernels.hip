@@ -1996,9 +1996,17 @@ static int resident_chunk_groups(int loads, int wpg, int nb) {
 
 // Wavefronts of the direct-to-LDS kernel resident per CU (queried once per
 // variant).
+// The direct-to-LDS kernel's wavefronts per CU, at most kMaxDmaWavesPerCu. With
+// records of 3-4 KB (60-70% sparsity) up to 13 fit a CU's LDS, but then a
+// layer of 14336 units no longer gives every wavefront 8 units and the planner
+// fell back to the four-wavefront kernel; at 7 per CU the 70B FFN takes 52.4
+// us at 60% and 50.1 at 70% (16 tokens) against 61.3 and 57.6 there, 67.6 and
+// 65.0 against 78.8 and 75.9 at 32 tokens.
+constexpr int kMaxDmaWavesPerCu = 7;
 static int resident_waves(int loads, int nb) {
     static std::atomic<int> cached[9][kMaxDmaTokenBlocks + 1];
-    return cached_occupancy(cached[loads][nb], reinterpret_cast<const void *>(dma_kernel(loads, nb)), kLanes);
+    const int r = cached_occupancy(cached[loads][nb], reinterpret_cast<const void *>(dma_kernel(loads, nb)), kLanes);
+    return r < kMaxDmaWavesPerCu ? r : kMaxDmaWavesPerCu;
 }
 
 static WaveKernelFn share_kernel(int loads, int nb) {
@@ -2012,16 +2020,11 @@ static WaveKernelFn share_kernel(int loads, int nb) {
         case 7: return spmm_share_kernel<7, NB>;      \
         default: return spmm_share_kernel<8, NB>;     \
     }
+    // 1 or 2 token blocks: from 3 the planner always takes the pipelined variant.
     if (nb == 1) {
         USP_SHARE(1)
     }
-    if (nb == 2) {
-        USP_SHARE(2)
-    }
-    if (nb == 3) {
-        USP_SHARE(3)
-    }
-    USP_SHARE(4)
+    USP_SHARE(2)
 #undef USP_SHARE
 }
 

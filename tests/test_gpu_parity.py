@@ -277,6 +277,22 @@ def test_dma_kernel_two_token_blocks_ragged(torch, usp):
     assert_close(Y, W, mask, X)
 
 
+# Records of fully dense tiles (8 KB of values) exceed the shared-decode
+# kernel's 8 KB slots once the mask is added, so from 33 tokens such a layer
+# stays on the direct-to-LDS kernel with 3-4 blocks per wavefront (the mask by
+# its own load) and token groups above 64: tolerance at 48 and 100 tokens.
+@pytest.mark.parametrize("N,route", [(48, "dma nb=3 tg=1"), (100, "dma nb=4 tg=2")])
+def test_dma_kernel_dense_records_token_groups(torch, usp, N, route):
+    W, mask, X = wl.make_random(36880, 8088, N, 1.0, seed=33 + N)
+    A = usp.SparseMatrix(W, mask)
+    plan = A.plan(N)
+    A.free()
+    print(f"case N={N}: {plan}", flush=True)
+    assert plan.startswith(route), plan
+    Y = run(torch, usp, W, mask, X)
+    assert_close(Y, W, mask, X)
+
+
 # The shared-decode kernel (33 to 256 tokens on large layers: four
 # wavefronts decode one record each into LDS, each multiplies all four by its
 # quarter of the tokens, X packed in product order first). Exact on small
