@@ -68,7 +68,11 @@ usp_status usp_encode(const uint16_t *W, int64_t ldw, const uint8_t *mask, int64
 
 /*
  * usp_workspace_size -- bytes of device workspace usp_spmm needs for this
- * handle and this N (0 when none). Returns 0 for a NULL handle.
+ * handle and this N (0 when none). Returns 0 for a NULL handle. The
+ * workspace holds the split rows' arrival counters and fp32 partials and,
+ * where the shared-decode kernel serves the call (33 to 256 tokens on large
+ * layers), a copy of X rearranged into the order its products read it
+ * (KT x 8 x ceil(N / 16) KB), rewritten by every such call.
  */
 size_t usp_workspace_size(const usp_matrix *A, int64_t N);
 
