@@ -1,11 +1,17 @@
 // usp_kernels.hip -- gfx950 kernels of the sparse product and their launchers.
 //
-// Four kernels share one decode; the planner (wave_kind, plan_wave, plan_pass)
+// Five kernels share one decode; the planner (wave_kind, plan_wave, plan_pass)
 // picks one by shape and token count:
-//   * spmm_dma_kernel (large layers, up to 256 tokens): one wavefront per
-//     workgroup streams a contiguous range of units (4 row blocks x 1 column
-//     tile), records moved straight into a ring of LDS slots, X in registers;
-//     more than 4 blocks of 16 tokens are split into token groups;
+//   * spmm_dma_kernel (large layers, up to 32 tokens; beyond, only records too
+//     large for the next kernel's slots): one wavefront per workgroup streams
+//     a contiguous range of units (4 row blocks x 1 column tile), records moved
+//     straight into a ring of LDS slots, X in registers; more than 4 blocks of
+//     16 tokens are split into token groups;
+//   * spmm_share_kernel and its pipelined variant spmm_pipe_kernel (large
+//     layers, 33 to 256 tokens): four wavefronts stream a range of units, each
+//     decodes one row block's record into a shared LDS buffer of A operands and
+//     multiplies all four by its quarter of the tokens, reading X packed in
+//     product order by pack_x_kernel;
 //   * spmm_chunk_kernel (small layers, up to 32 tokens): 4 or 8 row blocks x a
 //     chunk of 4 column tiles per workgroup, every record requested at once;
 //   * spmm_row_kernel (few row blocks, up to 16 tokens): one row block per
