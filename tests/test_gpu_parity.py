@@ -316,6 +316,20 @@ def test_share_kernel_exact(torch, usp, N):
     assert np.array_equal(Y, Yref)
 
 
+# 448 row sets on 512 resident workgroups (28672 x 5120 at 128 tokens): one
+# whole row set per workgroup, no partials. Exact on small integers.
+def test_share_kernel_whole_sets(torch, usp):
+    W, mask, X = wl.make_small_int(28672, 5120, 128, 0.5, seed=35, lo=-1, hi=1)
+    A = usp.SparseMatrix(W, mask)
+    plan = A.plan(128)
+    A.free()
+    print(f"case: {plan}", flush=True)
+    assert plan.startswith("share nb=2 grid=448"), plan
+    Y = run(torch, usp, W, mask, X)
+    Yref, _ = oracle.masked_gemm(W, mask, X)
+    assert np.array_equal(Y, Yref)
+
+
 # The pipelined variant at two blocks per wavefront, which the planner takes
 # on layers of fewer than 32 units per CU (5120 x 5120: 1600 units): exact at
 # 128 tokens, tolerance at 100 (the last wavefront's second block partly past
