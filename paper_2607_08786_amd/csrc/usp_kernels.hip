@@ -1119,21 +1119,22 @@ __global__ __launch_bounds__(kLanes) void spmm_dma_kernel(WaveArgs a, const uint
 }
 
 // ---------------------------------------------------------------------------
-// Shared-decode kernel (more than 64 tokens, and 33-64 on large layers).
+// Shared-decode kernel (33 to 256 tokens on large layers).
 //
 // A workgroup of four wavefronts streams a contiguous range of units (4 row
 // blocks x 1 column tile). Wavefront j owns row block j of every unit: it
-// moves that record into its own ring of S LDS slots (S - 1 units in flight
-// while one is decoded; S as deep as LDS allows), decodes it once into the 8 A operands of its steps and writes them to a
-// shared LDS buffer; after a barrier every wavefront multiplies all four
-// records' operands with the X of its own slice of tokens (NB blocks of 16,
-// up to 64 tokens, held in registers). Each record is decoded once however
-// many tokens there are: the direct-to-LDS kernel's token groups decoded every
-// record once per group (2 at 128 tokens, 4 at 256). The steps run outermost,
-// so each step's X operands are reloaded for the next unit as soon as its
-// last MFMA has been issued, 7 steps of MFMAs ahead of their use. Split row
-// sets are finished per wavefront through the token-group arrival protocol
-// (counter and partial slices per wavefront).
+// moves that record into its own two LDS ring slots (the transfer of unit
+// u + 2 is issued at the end of unit u), decodes it once into the 8 A operands
+// of its steps and writes them to a shared LDS buffer; after a barrier every
+// wavefront multiplies all four records' operands with the X of its own slice
+// of tokens (NB blocks of 16, up to 64 tokens, held in registers; X read from
+// the packed copy). Each record is decoded once however many tokens there
+// are: the direct-to-LDS kernel's token groups decoded every record once per
+// group (2 at 128 tokens, 4 at 256). The steps run outermost, so each step's X
+// operands are reloaded for the next unit as soon as its last MFMA has been
+// issued, 7 steps of MFMAs ahead of their use. Split row sets are finished per
+// wavefront through the token-group arrival protocol (counter and partial
+// slices per wavefront).
 // ---------------------------------------------------------------------------
 
 constexpr int kShareWaves = 4;  // wavefronts per workgroup = row blocks per unit
@@ -1144,7 +1145,7 @@ constexpr int kShareWaves = 4;  // wavefronts per workgroup = row blocks per uni
 // barrier; here this wavefront's LDS instructions complete (lgkmcnt) before
 // the barrier, and the clobber keeps the compiler from moving memory accesses
 // across it. Transfers into a ring slot are only ever read by the wavefront
-// that issued them, behind the compiler's own waits.
+// that issued them, behind its own hand-counted wait.
 __device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // ---------------------------------------------------------------------------
@@ -1219,9 +1220,12 @@ __device__ __attribute__((always_inline)) inline void static_for(F &&f, std::int
 // in flight while one is decoded).
 constexpr int kShareSlots = 2;
 
+// Up to 2 token blocks the launch bound asks for two workgroups per CU (at most
+// 256 registers: 238 at 2 blocks, no spills; 272 without the bound, one
+// workgroup per CU, 174 against 154 us on the 70B FFN at 128 tokens).
 template <int L, int NB>
-__global__ __launch_bounds__(kShareWaves *kLanes, NB <= 2 ? 2 : 1) void spmm_share_kernel(WaveArgs a, const uint32_t *__restrict__ off,
-                                                                         const uint8_t *__restrict__ stream) {
+__global__ __launch_bounds__(kShareWaves *kLanes, NB <= 2 ? 2 : 1) void spmm_share_kernel(
+    WaveArgs a, const uint32_t *__restrict__ off, const uint8_t *__restrict__ stream) {
     constexpr int R = kShareWaves;
     constexpr int S = kShareSlots;
     constexpr int kSlot = 1024 * L + 16;  // mask bytes, values and the decode's 12-byte overread
