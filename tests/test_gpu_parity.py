@@ -678,6 +678,7 @@ ROUTES = [
     ((36880, 8088, 16), "dma nb=1 tg=1"), ((36880, 8088, 32), "dma nb=2 tg=1"),
     ((36880, 8088, 48), "share nb=1"), ((36880, 8088, 64), "share nb=1"), ((36880, 8088, 100), "share nb=2"),
     ((8192, 28672, 128), "share nb=2"), ((28672, 8192, 256), "share nb=4"), ((5120, 5120, 128), "share nb=2"),
+    ((13824, 5120, 64), "share nb=1 grid=432"),
 ]
 
 
